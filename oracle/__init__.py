@@ -1,0 +1,133 @@
+"""fp64 CPU oracle for the Evoformer gated attention with pair bias.
+
+TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the benchmark's
+CPU-baseline leg are the only callers.  The product path (the HIP library and
+its Python binding) never imports this package, and this package imports
+nothing from the product.
+
+The arithmetic lives in ``evo_attn_oracle.c`` (plain loops, fp64, OpenMP over
+(row, head) pairs); this file only builds and calls it through ctypes.
+Every function cites what it computes in the C source header.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "evo_attn_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle_evoattn.so")
+
+_lib = None
+
+
+class _Dims(ctypes.Structure):
+    _fields_ = [("n_rows", ctypes.c_int64), ("seq_len", ctypes.c_int64),
+                ("n_heads", ctypes.c_int64), ("head_dim", ctypes.c_int64),
+                ("rows_per_bias", ctypes.c_int64)]
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (-O2, IEEE semantics, OpenMP)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-std=c11", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra",
+               "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build(force=True)
+        lib = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        lib.evo_oracle_fwd.argtypes = [ctypes.POINTER(_Dims), P, P, P, P, P, P, P, P]
+        lib.evo_oracle_bwd.argtypes = [ctypes.POINTER(_Dims)] + [P] * 12
+        lib.evo_oracle_probs.argtypes = [ctypes.POINTER(_Dims), P, P, P, P, ctypes.c_int64,
+                                         ctypes.c_int64, P]
+        for f in (lib.evo_oracle_fwd, lib.evo_oracle_bwd, lib.evo_oracle_probs):
+            f.restype = ctypes.c_int
+        lib.evo_oracle_threads.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def threads() -> int:
+    """OpenMP threads the oracle uses (OMP_NUM_THREADS, else all cores)."""
+    return int(_load().evo_oracle_threads())
+
+
+def _f64(x: Optional[np.ndarray]) -> Optional[np.ndarray]:
+    return None if x is None else np.ascontiguousarray(x, dtype=np.float64)
+
+
+def _ptr(x: Optional[np.ndarray]):
+    return None if x is None else x.ctypes.data_as(ctypes.c_void_p)
+
+
+def _dims(q: np.ndarray, rows_per_bias: int) -> _Dims:
+    N, L, H, d = q.shape
+    return _Dims(N, L, H, d, rows_per_bias)
+
+
+def _mask(m: Optional[np.ndarray]) -> Optional[np.ndarray]:
+    return None if m is None else np.ascontiguousarray(m, dtype=np.uint8)
+
+
+def forward(q, k, v, gate=None, bias=None, mask=None, rows_per_bias: Optional[int] = None
+            ) -> Tuple[np.ndarray, np.ndarray]:
+    """o [N,L,H,d] and lse [N,H,L] (natural log); fp64 inputs of shape [N,L,H,d]."""
+    q, k, v, gate, bias = map(_f64, (q, k, v, gate, bias))
+    mask = _mask(mask)
+    N, L, H, d = q.shape
+    rpb = rows_per_bias or max(N, 1)
+    out = np.zeros_like(q)
+    lse = np.zeros((N, H, L), np.float64)
+    dm = _dims(q, rpb)
+    st = _load().evo_oracle_fwd(ctypes.byref(dm), _ptr(q), _ptr(k), _ptr(v), _ptr(gate),
+                                _ptr(bias), _ptr(mask), _ptr(out), _ptr(lse))
+    if st:
+        raise ValueError("oracle forward failed with status %d" % st)
+    return out, lse
+
+
+def backward(q, k, v, dout, gate=None, bias=None, mask=None, rows_per_bias: Optional[int] = None):
+    """Gradients (dq, dk, dv, dgate or None, dbias or None)."""
+    q, k, v, dout, gate, bias = map(_f64, (q, k, v, dout, gate, bias))
+    mask = _mask(mask)
+    N, L, H, d = q.shape
+    rpb = rows_per_bias or max(N, 1)
+    dq, dk, dv = np.zeros_like(q), np.zeros_like(q), np.zeros_like(q)
+    dg = np.zeros_like(q) if gate is not None else None
+    db = np.zeros_like(bias) if bias is not None else None
+    dm = _dims(q, rpb)
+    st = _load().evo_oracle_bwd(ctypes.byref(dm), _ptr(q), _ptr(k), _ptr(v), _ptr(gate),
+                                _ptr(bias), _ptr(mask), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv),
+                                _ptr(dg), _ptr(db))
+    if st:
+        raise ValueError("oracle backward failed with status %d" % st)
+    return dq, dk, dv, dg, db
+
+
+def probs(q, k, bias=None, mask=None, row: int = 0, head: int = 0,
+          rows_per_bias: Optional[int] = None) -> np.ndarray:
+    """Softmax matrix P [L,L] of one (row, head)."""
+    q, k, bias = map(_f64, (q, k, bias))
+    mask = _mask(mask)
+    N, L, H, d = q.shape
+    rpb = rows_per_bias or max(N, 1)
+    P = np.zeros((L, L), np.float64)
+    dm = _dims(q, rpb)
+    st = _load().evo_oracle_probs(ctypes.byref(dm), _ptr(q), _ptr(k), _ptr(bias), _ptr(mask),
+                                  row, head, _ptr(P))
+    if st:
+        raise ValueError("oracle probs failed with status %d" % st)
+    return P

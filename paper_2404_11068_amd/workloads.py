@@ -1,0 +1,167 @@
+"""Seeded synthetic inputs for the Evoformer attention workloads.
+
+This module only draws random numbers and stores them; it holds none of the
+attention arithmetic.  Both the GPU path's tests/benchmark and the fp64
+oracle consume exactly the arrays produced here, so the two sides see
+identical bits.
+
+The shapes stand in for the Evoformer attention calls of an AlphaFold
+training step at the 256-residue crop (ScaleFold Section 2.1: four attention
+modules per Evoformer block -- MSA row attention with pair bias, MSA column
+attention, and triangle attention around the starting and ending node; the
+extra-MSA stack runs the same row attention over many more sequences).  No
+dataset is used: the OpenFold training data the paper trains on is replaced
+by these seeded draws.
+
+Recipe (one NumPy ``Generator(PCG64(seed))`` per workload; values drawn in
+fp64, rounded to fp32, and for bf16 workloads rounded again to bf16 with
+round-to-nearest-even).  Draw order: q, k, v, gate, bias, mask, dout.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Dict, Optional
+
+import numpy as np
+
+__all__ = ["Workload", "WORKLOADS", "by_name", "generate", "as_float64", "f32_to_bf16_bits"]
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    n_rows: int          # N: independent attention rows (batch * rows)
+    seq_len: int         # L: queries == keys
+    n_heads: int         # H
+    head_dim: int        # d
+    dtype: str           # "f32" or "bf16"
+    bias: bool           # pair bias [B,H,L,L] present
+    rows_per_bias: int   # rows sharing one bias plane
+    gate: bool = True
+    mask: str = "none"   # none | bernoulli | tail_pad | length
+    mask_p: float = 0.0  # drop probability for "bernoulli"
+    pad_max: int = 0     # "tail_pad": pad the last U{0..pad_max} keys
+    len_lo: int = 0      # "length": keep keys j < n, n ~ U{len_lo..len_hi}
+    len_hi: int = 0
+    qkv_scale: float = 1.0
+    seed: int = 0
+    description: str = ""
+
+    @property
+    def n_bias_planes(self) -> int:
+        return self.n_rows // self.rows_per_bias if self.bias else 0
+
+    @property
+    def tokens(self) -> int:
+        return self.n_rows * self.seq_len * self.n_heads * self.head_dim
+
+    @property
+    def score_elems(self) -> int:
+        return self.n_rows * self.n_heads * self.seq_len * self.seq_len
+
+    def flops_fwd(self) -> float:
+        """Dense count: QK^T and PV, 2 flop per multiply-add."""
+        return 4.0 * self.score_elems * self.head_dim
+
+    def flops_bwd(self) -> float:
+        """Dense count incl. the recomputed QK^T: QK^T, dP, dV, dQ, dK."""
+        return 10.0 * self.score_elems * self.head_dim
+
+    def with_rows(self, n_rows: int) -> "Workload":
+        rpb = self.rows_per_bias if self.rows_per_bias <= n_rows else n_rows
+        return dataclasses.replace(self, n_rows=n_rows, rows_per_bias=max(1, rpb))
+
+
+WORKLOADS = [
+    Workload("tri_tiny_f32", 32, 32, 4, 32, "f32", True, 32, mask="bernoulli", mask_p=0.10,
+             seed=1000,
+             description="tiny fp32 triangle-attention check: 32 rows x L=32, H=4, d=32, "
+                         "pair bias [4,32,32], 10% random key drop"),
+    Workload("msa_col_bf16", 256, 128, 8, 32, "bf16", False, 256, mask="tail_pad", pad_max=16,
+             qkv_scale=1.0 / math.sqrt(32.0), seed=1001,
+             description="MSA column attention: 256 residue columns x L=128 sequences, H=8, d=32, "
+                         "no bias, last U{0..16} sequences padded"),
+    Workload("msa_row_bias_bf16", 128, 256, 8, 32, "bf16", True, 128, mask="length",
+             len_lo=224, len_hi=256, seed=1002,
+             description="MSA row attention with pair bias: 128 rows x L=256 residues, H=8, d=32, "
+                         "bias [8,256,256] shared by all rows, keys beyond U{224..256} padded"),
+    Workload("tri_start_bf16", 256, 256, 4, 32, "bf16", True, 256, mask="length",
+             len_lo=224, len_hi=256, seed=1003,
+             description="triangle attention around the starting node: 256 rows x L=256, H=4, "
+                         "d=32, bias [4,256,256], keys beyond U{224..256} padded"),
+    Workload("extra_msa_bf16", 1024, 256, 8, 8, "bf16", True, 1024, mask="bernoulli",
+             mask_p=0.05, seed=1004,
+             description="extra-MSA row attention with pair bias: 1024 rows x L=256, H=8, d=8, "
+                         "bias [8,256,256], 5% random key drop"),
+]
+
+
+def by_name(name: str) -> Workload:
+    for w in WORKLOADS:
+        if w.name == name:
+            return w
+    raise KeyError(name)
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round fp32 values to bf16 (round to nearest, ties to even); returns uint16 bits."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    rounded = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    return rounded.astype(np.uint16)
+
+
+def as_float64(arr: np.ndarray, dtype: str) -> np.ndarray:
+    """Exact fp64 value of an array stored as fp32 values or bf16 bits."""
+    if dtype == "bf16":
+        assert arr.dtype == np.uint16
+        return (arr.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return np.asarray(arr, dtype=np.float32).astype(np.float64)
+
+
+def _store(x64: np.ndarray, dtype: str) -> np.ndarray:
+    x32 = x64.astype(np.float32)
+    return f32_to_bf16_bits(x32) if dtype == "bf16" else x32
+
+
+def _mask(w: Workload, rng: np.random.Generator, n_rows: int, L: int) -> Optional[np.ndarray]:
+    if w.mask == "none":
+        return None
+    if w.mask == "bernoulli":
+        keep = (rng.random((n_rows, L)) >= w.mask_p).astype(np.uint8)
+        empty = np.nonzero(keep.sum(axis=1) == 0)[0]
+        fix = rng.integers(0, L, size=len(empty)) if len(empty) else []
+        for r, j in zip(empty, fix):
+            keep[r, j] = 1
+        return keep
+    if w.mask == "tail_pad":
+        pad = int(rng.integers(0, w.pad_max + 1))
+        keep = np.ones((n_rows, L), np.uint8)
+        if pad:
+            keep[:, L - pad:] = 0
+        return keep
+    if w.mask == "length":
+        n = int(rng.integers(w.len_lo, w.len_hi + 1))
+        keep = np.zeros((n_rows, L), np.uint8)
+        keep[:, :n] = 1
+        return keep
+    raise ValueError(w.mask)
+
+
+def generate(w: Workload, seed: Optional[int] = None, with_dout: bool = True) -> Dict[str, np.ndarray]:
+    """Draw one input set.  Tensors q,k,v,gate,dout: [N,L,H,d]; bias: [B,H,L,L];
+    mask: [N,L] uint8 (1 = keep).  Stored as float32, or uint16 bf16 bits."""
+    rng = np.random.Generator(np.random.PCG64(w.seed if seed is None else seed))
+    N, L, H, d = w.n_rows, w.seq_len, w.n_heads, w.head_dim
+    shape = (N, L, H, d)
+    out: Dict[str, np.ndarray] = {}
+    for name in ("q", "k", "v"):
+        out[name] = _store(rng.standard_normal(shape) * w.qkv_scale, w.dtype)
+    out["gate"] = _store(rng.standard_normal(shape), w.dtype) if w.gate else None
+    if w.bias:
+        out["bias"] = _store(rng.standard_normal((w.n_bias_planes, H, L, L)), w.dtype)
+    else:
+        out["bias"] = None
+    out["mask"] = _mask(w, rng, N, L)
+    out["dout"] = _store(rng.standard_normal(shape), w.dtype) if with_dout else None
+    return out

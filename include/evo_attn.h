@@ -1,0 +1,140 @@
+/*
+ * evo_attn.h -- C ABI of the MI355X (gfx950) Evoformer attention library.
+ *
+ * The library computes the gated multi-head attention with pair bias that
+ * every Evoformer attention module runs (MSA row attention with pair bias,
+ * MSA column attention, extra-MSA row attention, triangle attention around
+ * the starting and the ending node), forward and backward:
+ *
+ *     o = sigmoid(g) * softmax(Q K^T / sqrt(d) + mask_bias + pair_bias) V
+ *
+ * ScaleFold (arXiv 2404.11068), Section 3.3, "Multi Head Attention": the
+ * pair-bias term is added to the logits before the softmax, which rules out a
+ * stock FlashAttention kernel; the paper fuses all of MHA into one
+ * FlashAttention-style kernel.  Section 2.1 lists the four Evoformer modules
+ * that contain this attention.  The exact semantics implemented here:
+ *
+ *   for row r (bias plane b = r / rows_per_bias), head h, query i, key j:
+ *     s[i][j] = (1/sqrt(d)) sum_c Q[r,i,h,c] K[r,j,h,c] + bias[b,h,i,j]
+ *     keys with key_mask[r,j] == 0 are excluded from the softmax
+ *     P       = softmax_j(s),  A[i] = sum_j P[i][j] V[r,j,h,:]
+ *     O       = sigmoid(G) * A         (no gate: O = A)
+ *     lse[r,h,i] = log(sum_{kept j} exp(s[i][j]))      (natural log, fp32)
+ *   A query whose keys are all masked gets O = 0, lse = -inf, zero gradients.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - All tensor pointers are DEVICE pointers owned by the caller.  The library
+ *   never allocates, frees or synchronises device memory, and keeps no
+ *   mutable global state; every call only enqueues kernels on `stream`
+ *   (a hipStream_t; NULL = the null stream), so calls may be captured into a
+ *   HIP graph.  Calls return as soon as the work is enqueued.
+ * - Token tensors Q, K, V, G, O, dO, dQ, dK, dV, dG share one layout: element
+ *   (r, t, h, c) lives at  base + r*stride_row + t*stride_tok + h*head_dim + c
+ *   (strides in ELEMENTS; the [H, d] block of a token is contiguous).  The
+ *   contiguous [N, L, H, d] layout has stride_row = L*H*d, stride_tok = H*d.
+ *   A transposed view (stride_row = H*d, stride_tok = L*H*d over an
+ *   [L, L, H, d] pair representation) gives triangle attention around the
+ *   ending node without a copy.
+ * - bias (if given) is contiguous [B, H, L, L] in the working dtype with
+ *   B = n_rows / rows_per_bias; dbias is contiguous [B, H, L, L] fp32.
+ * - key_mask (if given) is contiguous [N, L] bytes, nonzero = keep.
+ * - lse is contiguous [N, H, L] fp32.
+ * - Outputs are overwritten, never accumulated into.
+ * - Every argument is validated on the host before any HIP call; an invalid
+ *   call enqueues nothing and returns a nonzero status.  Nothing is printed,
+ *   thrown or aborted.  Non-finite input values are not checked.
+ */
+#ifndef EVO_ATTN_H
+#define EVO_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* working dtype of Q, K, V, G, O, bias, dO, dQ, dK, dV, dG */
+enum evo_attn_dtype {
+    EVO_DTYPE_F32 = 0,  /* IEEE fp32 throughout (fp32 MFMA) */
+    EVO_DTYPE_BF16 = 1  /* bf16 storage and MFMA inputs, fp32 accumulation */
+};
+
+enum evo_attn_status {
+    EVO_OK = 0,
+    EVO_ERR_INVALID_ARG = 1, /* null required pointer, negative size, bad rows_per_bias or strides */
+    EVO_ERR_UNSUPPORTED = 2, /* dtype, head_dim or seq_len outside the compiled set */
+    EVO_ERR_ALIGNMENT = 3,   /* token pointers/strides must allow 16-byte vector access */
+    EVO_ERR_WORKSPACE = 4,   /* workspace missing or smaller than evo_attn_bwd_workspace_size */
+    EVO_ERR_HIP = 5          /* a kernel launch failed (hipGetLastError after the launch) */
+};
+
+/* Compiled limits: head_dim in {8, 16, 32}; 0 <= seq_len <= EVO_ATTN_MAX_SEQ_LEN. */
+#define EVO_ATTN_MAX_SEQ_LEN 256
+
+typedef struct evo_attn_dims {
+    int32_t dtype;         /* enum evo_attn_dtype */
+    int32_t n_heads;       /* H >= 1 */
+    int32_t head_dim;      /* d */
+    int32_t reserved;      /* must be 0 */
+    int64_t n_rows;        /* N >= 0: independent attention rows (batch x rows) */
+    int64_t seq_len;       /* L >= 0: queries == keys */
+    int64_t rows_per_bias; /* >= 1; N % rows_per_bias == 0; ignored when bias is NULL */
+    int64_t stride_row;    /* elements between rows r and r+1 of every token tensor */
+    int64_t stride_tok;    /* elements between tokens t and t+1; >= H*d */
+} evo_attn_dims;
+
+/*
+ * Forward pass.
+ *   q, k, v : required token tensors (input)
+ *   gate    : gate logits (token tensor) or NULL for no gating
+ *   bias    : pair bias [B,H,L,L] or NULL
+ *   key_mask: [N,L] bytes or NULL (all keys kept)
+ *   out     : O (token tensor, output; must not alias an input)
+ *   lse     : [N,H,L] fp32 output, natural-log log-sum-exp of each query's
+ *             logits; required (the backward consumes it)
+ * Returns EVO_OK or an evo_attn_status.  An empty problem (N == 0 or L == 0)
+ * validates its arguments and returns EVO_OK without launching anything.
+ */
+int evo_attn_fwd(const evo_attn_dims *dims, const void *q, const void *k, const void *v,
+                 const void *gate, const void *bias, const uint8_t *key_mask, void *out,
+                 float *lse, void *stream);
+
+/*
+ * Bytes of device workspace evo_attn_bwd needs for these dims (0 if dims is
+ * invalid).  The value depends on the dims only; it may change between
+ * library versions, so query it rather than hard-coding it.
+ */
+size_t evo_attn_bwd_workspace_size(const evo_attn_dims *dims);
+
+/*
+ * Backward pass (recomputes the softmax from the saved lse).
+ *   q, k, v, gate, bias, key_mask : as passed to evo_attn_fwd
+ *   out, lse : the forward's outputs
+ *   dout     : dL/dO (token tensor)
+ *   dq, dk, dv : gradient outputs (token tensors)
+ *   dgate    : dL/dG output; NULL if and only if gate is NULL
+ *   dbias    : dL/dbias [B,H,L,L] fp32 output (summed over the rows sharing
+ *              each plane); NULL if and only if bias is NULL
+ *   workspace, workspace_bytes : caller-owned device scratch of at least
+ *              evo_attn_bwd_workspace_size(dims) bytes, 256-byte aligned;
+ *              its contents on entry do not matter
+ * The dbias reduction is deterministic: repeated calls give identical bits.
+ */
+int evo_attn_bwd(const evo_attn_dims *dims, const void *q, const void *k, const void *v,
+                 const void *gate, const void *bias, const uint8_t *key_mask, const void *out,
+                 const float *lse, const void *dout, void *dq, void *dk, void *dv, void *dgate,
+                 float *dbias, void *workspace, size_t workspace_bytes, void *stream);
+
+/* Static, human-readable text for a status code (never NULL). */
+const char *evo_attn_strerror(int status);
+
+/* Library ABI version (major * 10000 + minor * 100 + patch). */
+int evo_attn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EVO_ATTN_H */

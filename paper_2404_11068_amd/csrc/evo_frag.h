@@ -1,0 +1,190 @@
+// evo_frag.h -- gfx950 MFMA fragment helpers shared by the attention kernels.
+//
+// Every tile product in the kernels is a 32x32 output tile produced by one of
+//   v_mfma_f32_32x32x16_bf16   (bf16 inputs, k = 16)
+//   v_mfma_f32_32x32x8_bf16    (bf16 inputs, k = 8; head_dim 8)
+//   v_mfma_f32_32x32x2_f32     (fp32 inputs, k = 2)
+// Lane layout (wave64, lane l, half h = l / 32, col n = l % 32):
+//   A operand: row m = l % 32, k-slots h*kpl .. h*kpl + kpl - 1
+//   B operand: col n = l % 32, same k-slots
+//   D (16 fp32 regs): reg i holds D[rho(i, h)][n],  rho(i, h) = 8*(i/4) + 4*h + i%4
+//
+// Two index maps make the D layout directly reusable as an MFMA operand:
+//   * the rows of an A operand are loaded permuted by sig(m) (bits 2 and 3 of
+//     m swapped), so reg i of the product holds row krow(i, h) of the tile:
+//         krow(i, h) = 16*(i/8) + 8*h + i%8
+//   * a contraction over a 32-row block therefore uses, per lane half h, the
+//     rows {8h + s, 16 + 8h + s : s = 0..7} in register order -- the "k32"
+//     fragment below -- for both bf16 (2 MFMAs of k=16) and fp32 (16 MFMAs
+//     of k=2).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace evo {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef short short4v __attribute__((ext_vector_type(4)));
+
+struct bf16_t { uint16_t bits; };   // storage type of the bf16 path
+
+__device__ __forceinline__ int sig(int m) { return (m & ~0xC) | ((m & 4) << 1) | ((m & 8) >> 1); }
+__device__ __forceinline__ int krow(int i, int h) { return 16 * (i >> 3) + 8 * h + (i & 7); }
+
+__device__ __forceinline__ float bf2f(uint16_t u) { return __builtin_bit_cast(float, (uint32_t)u << 16); }
+__device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+
+// ---------------------------------------------------------------------------
+// per-dtype traits: element type, 16-byte vector width, MFMA wrappers
+template <typename T> struct Tr;
+
+template <> struct Tr<float> {
+    using elem = float;
+    static constexpr int VEC = 4;  // elements per 16 bytes
+    __device__ __forceinline__ static float to_f(float x) { return x; }
+    __device__ __forceinline__ static float from_f(float x) { return x; }
+    // k32 fragment: 16 floats, MFMA u contracts rows {krow(u,0), krow(u,1)}
+    struct K32 { float v[16]; };
+    __device__ __forceinline__ static void mma_k32(f32x16 &acc, const K32 &a, const K32 &b) {
+#pragma unroll
+        for (int u = 0; u < 16; ++u) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a.v[u], b.v[u], acc, 0, 0, 0);
+    }
+    __device__ __forceinline__ static K32 pack(const f32x16 &x) {
+        K32 r;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) r.v[i] = x[i];
+        return r;
+    }
+};
+
+template <> struct Tr<bf16_t> {
+    using elem = uint16_t;
+    static constexpr int VEC = 8;
+    __device__ __forceinline__ static float to_f(uint16_t x) { return bf2f(x); }
+    __device__ __forceinline__ static uint16_t from_f(float x) { return f2bf(x); }
+    struct K32 { bf16x8 v[2]; };
+    __device__ __forceinline__ static void mma_k32(f32x16 &acc, const K32 &a, const K32 &b) {
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.v[0], b.v[0], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.v[1], b.v[1], acc, 0, 0, 0);
+    }
+    __device__ __forceinline__ static K32 pack(const f32x16 &x) {
+        K32 r;
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+            r.v[0][s] = (__bf16)x[s];
+            r.v[1][s] = (__bf16)x[8 + s];
+        }
+        return r;
+    }
+};
+
+// Load a k32 fragment from a row of 32 consecutive elements (rows of the
+// contraction) -- the lane takes elements {8h+s, 16+8h+s}.
+template <typename T>
+__device__ __forceinline__ typename Tr<T>::K32 load_k32(const typename Tr<T>::elem *row32, int h) {
+    typename Tr<T>::K32 f;
+    if constexpr (sizeof(typename Tr<T>::elem) == 2) {
+        f.v[0] = *reinterpret_cast<const bf16x8 *>(row32 + 8 * h);
+        f.v[1] = *reinterpret_cast<const bf16x8 *>(row32 + 16 + 8 * h);
+    } else {
+        const float4 *p0 = reinterpret_cast<const float4 *>(row32 + 8 * h);
+        const float4 *p1 = reinterpret_cast<const float4 *>(row32 + 16 + 8 * h);
+        float4 a = p0[0], b = p0[1], c = p1[0], d = p1[1];
+        f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
+        f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
+        f.v[8] = c.x; f.v[9] = c.y; f.v[10] = c.z; f.v[11] = c.w;
+        f.v[12] = d.x; f.v[13] = d.y; f.v[14] = d.z; f.v[15] = d.w;
+    }
+    return f;
+}
+
+template <typename T>
+__device__ __forceinline__ typename Tr<T>::K32 zero_k32() {
+    typename Tr<T>::K32 f;
+    if constexpr (sizeof(typename Tr<T>::elem) == 2) {
+#pragma unroll
+        for (int s = 0; s < 8; ++s) { f.v[0][s] = (__bf16)0.0f; f.v[1][s] = (__bf16)0.0f; }
+    } else {
+#pragma unroll
+        for (int u = 0; u < 16; ++u) f.v[u] = 0.0f;
+    }
+    return f;
+}
+
+// ---------------------------------------------------------------------------
+// Channel-contraction fragments (QK^T and dA V^T): contraction over the D
+// channels of a token.  The channel order inside the contraction is free, so
+// each dtype uses the order that makes the lane's channels contiguous.
+template <typename T, int D> struct ChFrag;
+
+// fp32: D/2 MFMAs of k=2; lane half h holds channels h*D/2 + u, u < D/2
+template <int D> struct ChFrag<float, D> {
+    float v[D / 2];
+    __device__ __forceinline__ void load(const float *tok, int h) {
+#pragma unroll
+        for (int u = 0; u < D / 2; u += 4) {
+            float4 x = *reinterpret_cast<const float4 *>(tok + h * (D / 2) + u);
+            v[u] = x.x; v[u + 1] = x.y; v[u + 2] = x.z; v[u + 3] = x.w;
+        }
+    }
+    __device__ __forceinline__ void zero() {
+#pragma unroll
+        for (int u = 0; u < D / 2; ++u) v[u] = 0.0f;
+    }
+    __device__ __forceinline__ static void mma(f32x16 &acc, const ChFrag &a, const ChFrag &b) {
+#pragma unroll
+        for (int u = 0; u < D / 2; ++u) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a.v[u], b.v[u], acc, 0, 0, 0);
+    }
+};
+
+// bf16, D multiple of 16: D/16 MFMAs of k=16; lane half h holds channels 16kk + 8h + s
+template <int D> struct ChFrag<bf16_t, D> {
+    static_assert(D % 16 == 0, "bf16 head_dim 16/32 use k=16 MFMAs");
+    bf16x8 v[D / 16];
+    __device__ __forceinline__ void load(const uint16_t *tok, int h) {
+#pragma unroll
+        for (int kk = 0; kk < D / 16; ++kk) v[kk] = *reinterpret_cast<const bf16x8 *>(tok + 16 * kk + 8 * h);
+    }
+    __device__ __forceinline__ void zero() {
+#pragma unroll
+        for (int kk = 0; kk < D / 16; ++kk)
+#pragma unroll
+            for (int s = 0; s < 8; ++s) v[kk][s] = (__bf16)0.0f;
+    }
+    __device__ __forceinline__ static void mma(f32x16 &acc, const ChFrag &a, const ChFrag &b) {
+#pragma unroll
+        for (int kk = 0; kk < D / 16; ++kk)
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.v[kk], b.v[kk], acc, 0, 0, 0);
+    }
+};
+
+// bf16, D = 8: one MFMA of k=8; lane half h holds channels 4h + s, s < 4
+template <> struct ChFrag<bf16_t, 8> {
+    short4v v;
+    __device__ __forceinline__ void load(const uint16_t *tok, int h) {
+        v = *reinterpret_cast<const short4v *>(tok + 4 * h);
+    }
+    __device__ __forceinline__ void zero() { v = short4v{0, 0, 0, 0}; }
+    __device__ __forceinline__ static void mma(f32x16 &acc, const ChFrag &a, const ChFrag &b) {
+        acc = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(a.v, b.v, acc, 0, 0, 0);
+    }
+};
+
+__device__ __forceinline__ f32x16 zero16() {
+    f32x16 z;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) z[i] = 0.0f;
+    return z;
+}
+
+// XCD-aware unit index: consecutive units land on the same XCD (workgroups
+// are dispatched round-robin over the 8 XCDs), so the heads of one row share
+// that XCD's L2.
+__device__ __forceinline__ int64_t xcd_unit(int64_t b, int64_t nb) {
+    if (nb % 8 != 0) return b;
+    return (b % 8) * (nb / 8) + b / 8;
+}
+
+}  // namespace evo

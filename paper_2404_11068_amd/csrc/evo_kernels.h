@@ -1,0 +1,49 @@
+// evo_kernels.h -- internal launch interface between the C ABI layer and the
+// HIP kernels (not part of the public ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace evo {
+
+struct Problem {
+    int dtype;          // 0 = fp32, 1 = bf16
+    int H, D;
+    int64_t N, L, rpb;  // rpb: rows per bias plane
+    int64_t srow, stok; // token-tensor strides, elements
+};
+
+struct FwdPtrs {
+    const void *q, *k, *v, *g, *bias;
+    const uint8_t *mask;
+    void *out;
+    float *lse;
+};
+
+struct BwdPtrs {
+    const void *q, *k, *v, *g, *bias;
+    const uint8_t *mask;
+    const void *out;
+    const float *lse;
+    const void *dout;
+    void *dq, *dk, *dv, *dg;
+    float *dbias;
+};
+
+// Backward scratch plan: where each buffer lives inside the workspace.
+struct BwdPlan {
+    int64_t chunks;          // row chunks per bias plane (dBias partial planes per plane and head)
+    int64_t rows_per_chunk;  // rows summed by one dbias workgroup
+    int64_t n_wg;            // workgroups of the dbias kernel
+    size_t off_da, off_dsum, off_part, total;
+};
+
+BwdPlan plan_bwd(const Problem &p, bool has_bias);
+
+hipError_t launch_fwd(const Problem &p, const FwdPtrs &x, hipStream_t s);
+hipError_t launch_bwd(const Problem &p, const BwdPtrs &x, void *ws, const BwdPlan &plan,
+                      hipStream_t s);
+
+}  // namespace evo

@@ -1,0 +1,177 @@
+"""Python binding of the C ABI in include/evo_attn.h (argument marshalling only).
+
+Every step of the attention runs in the HIP library ``libevoattn.so``; this
+module only turns torch tensors into device pointers, the current torch
+stream into a hipStream_t, and nonzero status codes into exceptions.  If the
+library is missing, every call raises: there is no fallback path.
+
+Tensor conventions (torch, on the GPU):
+  q, k, v, gate, out, dout, dq, dk, dv, dgate : [N, L, H, d], the [H, d] block
+      of each token contiguous; all share one (row, token) stride pair, so a
+      transposed view ``x.transpose(0, 1)`` of an [L, L, H, d] pair
+      representation works for triangle attention around the ending node.
+  bias : [B, H, L, L] contiguous, B = N // rows_per_bias (rows r use plane r // rows_per_bias)
+  key_mask : [N, L] uint8 or bool (nonzero = keep)
+  lse : [N, H, L] float32;  dbias : [B, H, L, L] float32
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libevoattn.so")
+
+EVO_DTYPE_F32 = 0
+EVO_DTYPE_BF16 = 1
+EVO_ATTN_MAX_SEQ_LEN = 256
+
+_DTYPES = {torch.float32: EVO_DTYPE_F32, torch.bfloat16: EVO_DTYPE_BF16}
+
+
+class evo_attn_dims(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("n_rows", ctypes.c_int64), ("seq_len", ctypes.c_int64),
+                ("rows_per_bias", ctypes.c_int64), ("stride_row", ctypes.c_int64),
+                ("stride_tok", ctypes.c_int64)]
+
+
+class EvoAttnError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__("%s failed: status %d (%s)" % (where, status, evo_attn_strerror(status)))
+        self.status = status
+
+
+_lib = None
+
+
+def load_library():
+    """Load libevoattn.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libevoattn.so is not built (run __graft_entry__.build() or "
+                               "python -m paper_2404_11068_amd.build); no fallback exists")
+        lib = ctypes.CDLL(LIB_PATH)
+        P = ctypes.c_void_p
+        D = ctypes.POINTER(evo_attn_dims)
+        lib.evo_attn_fwd.argtypes = [D, P, P, P, P, P, P, P, P, P]
+        lib.evo_attn_fwd.restype = ctypes.c_int
+        lib.evo_attn_bwd_workspace_size.argtypes = [D]
+        lib.evo_attn_bwd_workspace_size.restype = ctypes.c_size_t
+        lib.evo_attn_bwd.argtypes = [D] + [P] * 15 + [ctypes.c_size_t, P]
+        lib.evo_attn_bwd.restype = ctypes.c_int
+        lib.evo_attn_strerror.argtypes = [ctypes.c_int]
+        lib.evo_attn_strerror.restype = ctypes.c_char_p
+        lib.evo_attn_version.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def evo_attn_strerror(status: int) -> str:
+    return load_library().evo_attn_strerror(int(status)).decode()
+
+
+def evo_attn_version() -> int:
+    return int(load_library().evo_attn_version())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def make_dims(q: torch.Tensor, rows_per_bias: Optional[int] = None) -> evo_attn_dims:
+    if q.dim() != 4:
+        raise ValueError("token tensors are [N, L, H, d]")
+    if q.dtype not in _DTYPES:
+        raise ValueError("dtype must be float32 or bfloat16")
+    N, L, H, d = q.shape
+    if q.stride(3) != 1 or (H > 1 and q.stride(2) != d):
+        raise ValueError("the [H, d] block of each token must be contiguous")
+    return evo_attn_dims(_DTYPES[q.dtype], H, d, 0, N, L,
+                         rows_per_bias if rows_per_bias is not None else max(N, 1),
+                         q.stride(0), q.stride(1))
+
+
+def _same_layout(ref: torch.Tensor, *ts):
+    for t in ts:
+        if t is None:
+            continue
+        if t.shape != ref.shape or t.stride() != ref.stride() or t.dtype != ref.dtype:
+            raise ValueError("token tensors must share shape, strides and dtype")
+
+
+def _mask_u8(m: Optional[torch.Tensor]) -> Optional[torch.Tensor]:
+    if m is None:
+        return None
+    if m.dtype == torch.bool:
+        m = m.to(torch.uint8)
+    if m.dtype != torch.uint8 or not m.is_contiguous():
+        raise ValueError("key_mask must be a contiguous [N, L] uint8/bool tensor")
+    return m
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def evo_attn_fwd(q, k, v, gate=None, bias=None, key_mask=None, *, rows_per_bias=None,
+                 out=None, lse=None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Forward pass; returns (out, lse).  See include/evo_attn.h."""
+    lib = load_library()
+    _same_layout(q, k, v, gate)
+    dims = make_dims(q, rows_per_bias)
+    N, L, H, d = q.shape
+    if out is None:
+        out = torch.empty_strided(q.shape, q.stride(), dtype=q.dtype, device=q.device)
+    _same_layout(q, out)
+    if lse is None:
+        lse = torch.empty((N, H, L), dtype=torch.float32, device=q.device)
+    key_mask = _mask_u8(key_mask)
+    st = lib.evo_attn_fwd(ctypes.byref(dims), _ptr(q), _ptr(k), _ptr(v), _ptr(gate), _ptr(bias),
+                          _ptr(key_mask), _ptr(out), _ptr(lse), _stream(stream))
+    if st:
+        raise EvoAttnError(st, "evo_attn_fwd")
+    return out, lse
+
+
+def evo_attn_bwd_workspace_size(q: torch.Tensor, rows_per_bias=None) -> int:
+    dims = make_dims(q, rows_per_bias)
+    return int(load_library().evo_attn_bwd_workspace_size(ctypes.byref(dims)))
+
+
+def evo_attn_bwd(q, k, v, gate, bias, key_mask, out, lse, dout, *, rows_per_bias=None,
+                 dq=None, dk=None, dv=None, dgate=None, dbias=None, workspace=None, stream=None):
+    """Backward pass; returns (dq, dk, dv, dgate or None, dbias or None)."""
+    lib = load_library()
+    _same_layout(q, k, v, gate, out, dout)
+    dims = make_dims(q, rows_per_bias)
+
+    def like_q():
+        return torch.empty_strided(q.shape, q.stride(), dtype=q.dtype, device=q.device)
+
+    dq = like_q() if dq is None else dq
+    dk = like_q() if dk is None else dk
+    dv = like_q() if dv is None else dv
+    if gate is not None and dgate is None:
+        dgate = like_q()
+    if bias is not None and dbias is None:
+        dbias = torch.empty(bias.shape, dtype=torch.float32, device=q.device)
+    _same_layout(q, dq, dk, dv, dgate)
+    need = int(lib.evo_attn_bwd_workspace_size(ctypes.byref(dims)))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    key_mask = _mask_u8(key_mask)
+    st = lib.evo_attn_bwd(ctypes.byref(dims), _ptr(q), _ptr(k), _ptr(v), _ptr(gate), _ptr(bias),
+                          _ptr(key_mask), _ptr(out), _ptr(lse), _ptr(dout), _ptr(dq), _ptr(dk),
+                          _ptr(dv), _ptr(dgate), _ptr(dbias), _ptr(workspace),
+                          ctypes.c_size_t(workspace.numel() * workspace.element_size()),
+                          _stream(stream))
+    if st:
+        raise EvoAttnError(st, "evo_attn_bwd")
+    return dq, dk, dv, dgate, dbias

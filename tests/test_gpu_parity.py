@@ -1,0 +1,143 @@
+"""GPU parity: the HIP library (through its C ABI) against the fp64 oracle,
+element by element on identical seeded inputs.
+
+* every workload at its full size (all outputs, all elements);
+* small shapes that span several 32-key tiles with ragged tails, every head
+  dim, fp32 and bf16, with and without gate / bias / mask, several bias planes;
+* the ending-node layout (a transposed view, no copy);
+* edge cases: one key, fully masked rows, empty problems, maximum seq_len;
+* properties: exact zeros at masked keys, bitwise-repeatable backward,
+  non-default stream, rows independent.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2404_11068_amd import evo_attn as ea
+from paper_2404_11068_amd import workloads as W
+from tests.parity_util import compare, gpu_run, make_inputs, oracle_run, to_device
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("name", [w.name for w in W.WORKLOADS])
+def test_full_workload_parity(name):
+    w = W.by_name(name)
+    x = W.generate(w)
+    print("\n[case] full workload", name, flush=True)
+    got = gpu_run(x, w.dtype, w.rows_per_bias)
+    ref = oracle_run(x, w.dtype, w.rows_per_bias)
+    rep = compare(got, ref, w.dtype, label=name)
+    for k, v in rep.items():
+        print("  %-6s max_abs %.3e  rel_norm %.3e" % (k, v["max_abs"], v["rel_norm"]))
+
+
+SMALL = [
+    # N, L, H, d, dtype, kwargs
+    (3, 1, 2, 8, "bf16", dict(mask="none")),
+    (4, 5, 2, 16, "bf16", dict()),
+    (4, 33, 3, 32, "bf16", dict(rpb=2)),
+    (2, 63, 2, 8, "bf16", dict(gate=False)),
+    (3, 100, 2, 32, "bf16", dict(bias=False, mask="tail_pad")),
+    (2, 129, 1, 16, "bf16", dict(mask="length")),
+    (2, 200, 2, 32, "bf16", dict(rpb=1)),
+    (2, 255, 1, 8, "bf16", dict(p=0.3)),
+    (2, 256, 2, 32, "bf16", dict(mask="none", gate=False, bias=False)),
+    (3, 7, 2, 8, "f32", dict()),
+    (2, 37, 2, 16, "f32", dict(rpb=1)),
+    (2, 96, 2, 32, "f32", dict(mask="length")),
+    (2, 128, 1, 32, "f32", dict(gate=False)),
+    (2, 250, 1, 16, "f32", dict(p=0.2)),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=lambda c: "N%dL%dH%dd%d_%s_%s" % (c[:5] + (
+    "-".join("%s=%s" % kv for kv in sorted(c[5].items())) or "default",)))
+def test_small_ragged_parity(case):
+    N, L, H, d, dtype, kw = case
+    w, x = make_inputs(N, L, H, d, dtype, seed=7 + L, **kw)
+    print("\n[case]", case, flush=True)
+    got = gpu_run(x, dtype, w.rows_per_bias)
+    ref = oracle_run(x, dtype, w.rows_per_bias)
+    compare(got, ref, dtype, label=str(case))
+
+
+def test_ending_node_transposed_view():
+    """Triangle attention around the ending node: rows are the columns of the
+    pair representation, passed as a strided view without a copy."""
+    L, H, d = 64, 4, 32
+    w, x = make_inputs(L, L, H, d, "bf16", seed=11, mask="length")
+    print("\n[case] ending-node view", flush=True)
+    # the pair representation z[i, j] holds row j, token i: build it so that
+    # z.transpose(0, 1) is the [N=L, L, H, d] logical tensor of x
+    def view(t):
+        z = t.transpose(0, 1).contiguous()      # physical [L(token), L(row), H, d]
+        v = z.transpose(0, 1)                   # logical [row, token, H, d], strided
+        assert not v.is_contiguous()
+        return v
+    got = gpu_run(x, "bf16", w.rows_per_bias, view=view)
+    ref = oracle_run(x, "bf16", w.rows_per_bias)
+    compare(got, ref, "bf16", label="ending-node")
+
+
+def test_fully_masked_rows_are_zero():
+    N, L, H, d = 4, 40, 2, 16
+    w, x = make_inputs(N, L, H, d, "bf16", seed=3)
+    x["mask"][1] = 0
+    x["mask"][3] = 0
+    print("\n[case] fully masked rows", flush=True)
+    got = gpu_run(x, "bf16", w.rows_per_bias)
+    assert (got["out"][[1, 3]] == 0).all()
+    assert np.isneginf(got["lse"][[1, 3]]).all()
+    for n in ("dq", "dk", "dv", "dgate"):
+        assert (got[n][[1, 3]] == 0).all(), n
+    ref = oracle_run(x, "bf16", w.rows_per_bias)
+    compare(got, ref, "bf16", label="fully-masked")
+
+
+def test_masked_keys_get_exact_zero_gradients():
+    w, x = make_inputs(3, 90, 2, 32, "bf16", seed=5, p=0.3)
+    got = gpu_run(x, "bf16", w.rows_per_bias)
+    masked = x["mask"] == 0
+    assert masked.any()
+    assert (got["dk"][masked] == 0).all() and (got["dv"][masked] == 0).all()
+
+
+def test_empty_problems_are_noops():
+    for shape in [(0, 16, 2, 32), (3, 0, 2, 32)]:
+        q = torch.zeros(shape, dtype=torch.bfloat16, device="cuda")
+        out, lse = ea.evo_attn_fwd(q, q, q)
+        dq, dk, dv, dg, db = ea.evo_attn_bwd(q, q, q, None, None, None, out, lse, q)
+        torch.cuda.synchronize()
+        assert out.numel() == 0 and dq.numel() == 0
+
+
+def test_backward_is_bitwise_repeatable_and_stream_ordered():
+    w = W.by_name("msa_row_bias_bf16").with_rows(16)
+    x = W.generate(w)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        a = gpu_run(x, w.dtype, w.rows_per_bias, stream=s)
+        b = gpu_run(x, w.dtype, w.rows_per_bias, stream=s)
+    for n in a:
+        if a[n] is not None:
+            assert np.array_equal(a[n], b[n], equal_nan=True), n
+
+
+def test_rows_are_independent():
+    w, x = make_inputs(6, 70, 2, 16, "bf16", seed=9, rpb=6)
+    full = gpu_run(x, "bf16", 6)
+    sub = {k: (None if v is None else (v[2:4] if k not in ("bias",) else v)) for k, v in x.items()}
+    part = gpu_run(sub, "bf16", 2)
+    for n in ("out", "lse", "dq", "dk", "dv", "dgate"):
+        np.testing.assert_array_equal(part[n], full[n][2:4])
+
+
+def test_unsupported_shapes_raise():
+    q = torch.zeros((2, 300, 2, 32), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(ea.EvoAttnError) as e:
+        ea.evo_attn_fwd(q, q, q)
+    assert e.value.status == 2
+    q = torch.zeros((2, 16, 2, 24), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(ea.EvoAttnError):
+        ea.evo_attn_fwd(q, q, q)

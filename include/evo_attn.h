@@ -95,7 +95,8 @@ typedef struct evo_attn_dims {
  *   lse     : [N,H,L] fp32 output, natural-log log-sum-exp of each query's
  *             logits; required (the backward consumes it)
  * Returns EVO_OK or an evo_attn_status.  An empty problem (N == 0 or L == 0)
- * validates its arguments and returns EVO_OK without launching anything.
+ * validates dims and returns EVO_OK without launching anything or looking at
+ * any pointer (which may then be NULL); the same holds for evo_attn_bwd.
  */
 int evo_attn_fwd(const evo_attn_dims *dims, const void *q, const void *k, const void *v,
                  const void *gate, const void *bias, const uint8_t *key_mask, void *out,
@@ -120,7 +121,9 @@ size_t evo_attn_bwd_workspace_size(const evo_attn_dims *dims);
  *   workspace, workspace_bytes : caller-owned device scratch of at least
  *              evo_attn_bwd_workspace_size(dims) bytes, 256-byte aligned;
  *              its contents on entry do not matter
- * The dbias reduction is deterministic: repeated calls give identical bits.
+ * Repeated calls give bitwise identical dk, dv, dgate and dbias (dbias is a
+ * fixed-order two-step reduction).  dq is summed over key tiles with on-chip
+ * float atomics, so its last bit may vary between calls.
  */
 int evo_attn_bwd(const evo_attn_dims *dims, const void *q, const void *k, const void *v,
                  const void *gate, const void *bias, const uint8_t *key_mask, const void *out,

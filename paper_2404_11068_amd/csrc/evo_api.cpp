@@ -70,12 +70,12 @@ int evo_attn_fwd(const evo_attn_dims *dims, const void *q, const void *k, const 
     evo::Problem p;
     int st = check_dims(dims, bias != nullptr, &p);
     if (st) return st;
+    if (p.N == 0 || p.L == 0) return EVO_OK;  // nothing is read or written
     if (!q || !k || !v || !out || !lse) return EVO_ERR_INVALID_ARG;
     if (out == q || out == k || out == v || (gate && out == gate)) return EVO_ERR_INVALID_ARG;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) || (gate && !aligned16(gate)) ||
         (bias && !aligned16(bias)) || !aligned4(lse))
         return EVO_ERR_ALIGNMENT;
-    if (p.N == 0 || p.L == 0) return EVO_OK;
     evo::FwdPtrs x{q, k, v, gate, bias, key_mask, out, lse};
     hipError_t e = evo::launch_fwd(p, x, (hipStream_t)stream);
     return e == hipSuccess ? EVO_OK : EVO_ERR_HIP;
@@ -98,10 +98,10 @@ int evo_attn_bwd(const evo_attn_dims *dims, const void *q, const void *k, const 
     evo::Problem p;
     int st = check_dims(dims, bias != nullptr, &p);
     if (st) return st;
+    if (p.N == 0 || p.L == 0) return EVO_OK;  // nothing is read or written
     if (!q || !k || !v || !out || !lse || !dout || !dq || !dk || !dv) return EVO_ERR_INVALID_ARG;
     if ((gate == nullptr) != (dgate == nullptr) || (bias == nullptr) != (dbias == nullptr))
         return EVO_ERR_INVALID_ARG;
-    if (dims->dtype == EVO_DTYPE_F32 && dims->head_dim == 32 && dims->seq_len > 128) return EVO_ERR_UNSUPPORTED;
     const void *tok[] = {q, k, v, out, dout, dq, dk, dv};
     for (const void *t : tok)
         if (!aligned16(t)) return EVO_ERR_ALIGNMENT;
@@ -109,7 +109,6 @@ int evo_attn_bwd(const evo_attn_dims *dims, const void *q, const void *k, const 
         (dbias && !aligned16(dbias)) || !aligned4(lse))
         return EVO_ERR_ALIGNMENT;
     const evo::BwdPlan plan = evo::plan_bwd(p, bias != nullptr);
-    if (p.N == 0 || p.L == 0) return EVO_OK;
     if (!workspace || workspace_bytes < plan.total || ((uintptr_t)workspace & 255u) != 0) return EVO_ERR_WORKSPACE;
     evo::BwdPtrs x{q, k, v, gate, bias, key_mask, out, lse, dout, dq, dk, dv, dgate, dbias};
     hipError_t e = evo::launch_bwd(p, x, workspace, plan, (hipStream_t)stream);

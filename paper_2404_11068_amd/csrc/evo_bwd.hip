@@ -2,31 +2,30 @@
 //
 // Recompute-based backward of o = sigmoid(g) * softmax(s) V with
 // s = Q K^T / sqrt(d) + bias + mask (ScaleFold Section 3.3, "Multi Head
-// Attention"; the kernel recomputes the probabilities from the saved
-// log-sum-exp instead of storing them):
+// Attention"; the probabilities are recomputed from the saved log-sum-exp):
 //   dA = dO sigmoid(g),  dG = dO o (1 - sigmoid(g)),  Dsum_i = sum_c dO_ic o_ic
 //   P  = exp(s - lse),   dP = dA V^T,   dS = P (dP - Dsum)
 //   dV = P^T dA,  dK = dS^T Q / sqrt(d),  dQ = dS K / sqrt(d),
 //   dBias[plane] = sum over the plane's rows of dS.
 //
-// Four kernels:
-//   prep   -- elementwise: dA (to workspace), Dsum (to workspace), dG.
-//   main   -- one workgroup per (row, head); wave w owns key tile w (32 keys)
-//             and loops over the query tiles.  dK and dV of the tile finish
-//             in the wave's registers, dQ is summed over the key tiles with
-//             LDS float atomics.
-//   dbias  -- one workgroup per (bias plane, head, key tile, chunk of rows):
-//             recomputes dS for its 32 keys x all queries over the chunk's
-//             rows, accumulating in registers, and writes one partial plane
-//             tile per chunk.
-//   reduce -- sums the partial planes of each (plane, head) into dbias.
-// dBias gets its own kernel because a register accumulator for a whole
-// (head, L x L) plane does not fit beside the dQ/dK/dV working set; the
-// recompute costs two small MFMAs and one exp per logit.  The reduction is a
-// fixed-order two-step reduction (register accumulation, then a sum over
-// partial planes), so results are bitwise repeatable; global float atomics
-// are avoided (they sustain only a few hundred million adds per second on
-// this part).
+// dK and dV are sums over queries, dQ a sum over keys and dBias a sum over
+// rows.  No single tiling finishes all three in registers, and global or LDS
+// float atomics are slow on this part (a few hundred million adds per
+// second; LDS atomics left a first version of this kernel waiting on LDS
+// half of the time), so the work is split into two passes that each
+// recompute P and dS in the orientation their sums need:
+//
+//   kv      one workgroup per (row, head); wave w owns key tile w (32 keys),
+//           lane = key, registers = queries.  dK and dV finish in registers.
+//           It also does the elementwise part (dA, Dsum, dG) while staging,
+//           and leaves dA and Dsum in the workspace for the second pass.
+//   qbias   one workgroup per (bias plane, head, 32-query tile, chunk of
+//           rows); wave w owns key tile w, lane = query, registers = keys.
+//           dQ is summed over the waves through LDS in a fixed order; dS is
+//           accumulated over the chunk's rows in registers and written once
+//           per chunk as a partial dBias tile.
+//   reduce  sums the partial dBias planes in chunk order.
+// Every sum has a fixed order, so all outputs are bitwise repeatable.
 #include <math.h>
 #include <stdlib.h>
 
@@ -41,408 +40,437 @@ constexpr float kLog2e = 1.4426950408889634f;
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// ---------------------------------------------------------------------------
-struct PrepArgs {
-    const void *out, *dout, *g;
-    void *da;      // workspace [N][L][H][D]
-    float *dsum;   // workspace [N][H][L]
-    void *dg;
-    int64_t N, L, srow, stok;
-    int H;
-};
-
-template <typename T, int D>
-__global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
+// 8 consecutive values row[j0 .. j0+7] as fp32; entries at or beyond n read as 0
+template <typename T>
+__device__ __forceinline__ void load_row8(const typename Tr<T>::elem *row, int j0, int n, bool vec_ok,
+                                          float *out8) {
     using E = typename Tr<T>::elem;
-    constexpr int VEC = Tr<T>::VEC;
-    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // (r, t, h)
-    const int64_t total = a.N * a.L * a.H;
-    if (idx >= total) return;
-    const int h = (int)(idx % a.H);
-    const int64_t rt = idx / a.H;
-    const int64_t t = rt % a.L, r = rt / a.L;
-    const int64_t tok = r * a.srow + t * a.stok + (int64_t)h * D;
-    const E *O = (const E *)a.out + tok;
-    const E *dO = (const E *)a.dout + tok;
-    const E *G = a.g ? (const E *)a.g + tok : nullptr;
-    E *dA = (E *)a.da + idx * D;
-    E *dG = a.dg ? (E *)a.dg + tok : nullptr;
-    float dsum = 0.0f;
+    if (vec_ok && j0 + 8 <= n) {
+        if constexpr (sizeof(E) == 2) {
+            uint4 u = *reinterpret_cast<const uint4 *>(row + j0);
+            uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
-    for (int c0 = 0; c0 < D; c0 += VEC) {
-        uint4 ov = *reinterpret_cast<const uint4 *>(O + c0);
-        uint4 dov = *reinterpret_cast<const uint4 *>(dO + c0);
-        uint4 gv = make_uint4(0, 0, 0, 0);
-        if (G) gv = *reinterpret_cast<const uint4 *>(G + c0);
-        const E *oe = reinterpret_cast<const E *>(&ov);
-        const E *de = reinterpret_cast<const E *>(&dov);
-        const E *ge = reinterpret_cast<const E *>(&gv);
-        uint4 dav, dgv;
-        E *dae = reinterpret_cast<E *>(&dav);
-        E *dge = reinterpret_cast<E *>(&dgv);
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) {
-            const float o = Tr<T>::to_f(oe[e]), d = Tr<T>::to_f(de[e]);
-            dsum = __builtin_fmaf(d, o, dsum);
-            if (G) {
-                const float sg = 1.0f / (1.0f + __builtin_amdgcn_exp2f(-Tr<T>::to_f(ge[e]) * kLog2e));
-                dae[e] = Tr<T>::from_f(d * sg);
-                dge[e] = Tr<T>::from_f(d * o * (1.0f - sg));
-            } else {
-                dae[e] = de[e];  // no gate: dA = dO
+            for (int s = 0; s < 4; ++s) {
+                out8[2 * s] = __builtin_bit_cast(float, w[s] << 16);
+                out8[2 * s + 1] = __builtin_bit_cast(float, w[s] & 0xffff0000u);
             }
+        } else {
+            float4 a = *reinterpret_cast<const float4 *>(row + j0);
+            float4 b = *reinterpret_cast<const float4 *>(row + j0 + 4);
+            out8[0] = a.x; out8[1] = a.y; out8[2] = a.z; out8[3] = a.w;
+            out8[4] = b.x; out8[5] = b.y; out8[6] = b.z; out8[7] = b.w;
         }
-        *reinterpret_cast<uint4 *>(dA + c0) = dav;
-        if (dG) *reinterpret_cast<uint4 *>(dG + c0) = dgv;
+    } else {
+#pragma unroll
+        for (int s = 0; s < 8; ++s) out8[s] = (j0 + s < n) ? Tr<T>::to_f(row[j0 + s]) : 0.0f;
     }
-    a.dsum[(r * a.H + h) * a.L + t] = dsum;
 }
 
 // ---------------------------------------------------------------------------
-struct MainArgs {
-    const void *q, *k, *v, *bias;
+// biasT[p][j][i] = bias[p][i][j] for every (plane, head) p; 32x32 tiles via LDS
+template <typename E>
+__global__ void __launch_bounds__(256) transpose_kernel(const E *__restrict__ src, E *__restrict__ dst, int64_t L,
+                                                     int64_t tiles) {
+    __shared__ E tile[32][33];
+    const int64_t blk = blockIdx.x;
+    const int64_t p = blk / (tiles * tiles);
+    const int64_t tij = blk % (tiles * tiles);
+    const int64_t i0 = (tij / tiles) * 32, j0 = (tij % tiles) * 32;
+    const E *s = src + p * L * L;
+    E *d = dst + p * L * L;
+    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+    for (int k = ty; k < 32; k += 8) {
+        const int64_t i = i0 + k, j = j0 + tx;
+        if (i < L && j < L) tile[k][tx] = s[i * L + j];
+    }
+    __syncthreads();
+    for (int k = ty; k < 32; k += 8) {
+        const int64_t j = j0 + k, i = i0 + tx;
+        if (i < L && j < L) d[j * L + i] = tile[tx][k];
+    }
+}
+
+// ---------------------------------------------------------------------------
+struct KvArgs {
+    const void *q, *k, *v, *g, *out, *dout, *biasT;
     const uint8_t *mask;
     const float *lse;
-    const void *da;
-    const float *dsum;
-    void *dq, *dk, *dv;
+    void *dk, *dv, *dg;
+    void *da;     // workspace [N][H][L][D]
+    float *dsum;  // workspace [N][H][L]
     int64_t L, rpb, srow, stok;
     int H;
     float scale;
 };
 
 template <typename T, int D, int NKT>
-__global__ void __launch_bounds__(NKT * 64) main_kernel(MainArgs a) {
+__global__ void __launch_bounds__(NKT * 64, (NKT == 8 && sizeof(typename Tr<T>::elem) == 2) ? 4 : 2) kv_kernel(KvArgs a) {
     using E = typename Tr<T>::elem;
     using K32 = typename Tr<T>::K32;
     constexpr int VEC = Tr<T>::VEC;
+    constexpr int CPT = D / VEC;     // 16-byte chunks per token
     constexpr int LP = NKT * 32;
     constexpr int NT = NKT * 64;
     constexpr int RSTR = D + VEC;    // row-major LDS stride
     constexpr int TSTR = LP + VEC;   // transposed LDS stride
-    constexpr int QSTR = D + 1;      // dQ accumulator stride (odd: spreads LDS banks)
-    constexpr int SSTR = 32 + VEC;   // dS scratch stride
     __shared__ __attribute__((aligned(16))) E q_lds[LP * RSTR];
     __shared__ __attribute__((aligned(16))) E da_lds[LP * RSTR];
     __shared__ __attribute__((aligned(16))) E qt_lds[D * TSTR];
     __shared__ __attribute__((aligned(16))) E dat_lds[D * TSTR];
     __shared__ __attribute__((aligned(16))) float lse2_lds[LP];
     __shared__ __attribute__((aligned(16))) float dsum_lds[LP];
-    __shared__ float dq_acc[LP * QSTR];
-    __shared__ __attribute__((aligned(16))) E dsc[NKT * 32 * SSTR];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int h2 = lane >> 5, n = lane & 31;
     const int L = (int)a.L;
-    // unit -> (row, head), head fastest so the heads of one row run back to
-    // back on one XCD
-    const int64_t unit = xcd_unit(blockIdx.x, gridDim.x);
+    const int64_t unit = xcd_unit(blockIdx.x, gridDim.x);  // (row, head), head fastest
     const int hh = (int)(unit % a.H);
     const int64_t r = unit / a.H;
     const int64_t b = r / a.rpb;
+    const int64_t base = r * a.srow + (int64_t)hh * D;
+    const int64_t rh = r * a.H + hh;
 
-    const int kt = wave;
-    const int key = kt * 32 + n;
-    const int krow_sig = sig(n);                 // permuted operand row of this lane
-    const E *bias_plane = a.bias ? (const E *)a.bias + (b * a.H + hh) * (int64_t)L * L : nullptr;
-
-    for (int i = tid; i < LP * QSTR; i += NT) dq_acc[i] = 0.0f;
-
+    // ---- stage Q and dA (both layouts); dA, Dsum and dG come from dO, O, G here
     {
-        const int64_t base = r * a.srow + (int64_t)hh * D;
-        // ---- stage Q and dA in both layouts, lse (log2 units) and Dsum
         const E *Q = (const E *)a.q + base;
-        const E *dA = (const E *)a.da + ((r * L) * a.H + hh) * D;
-        for (int idx = tid; idx < LP * (D / VEC); idx += NT) {
-            const int t = idx / (D / VEC), c = (idx % (D / VEC)) * VEC;
-            uint4 qv = make_uint4(0, 0, 0, 0), av = make_uint4(0, 0, 0, 0);
-            if (t < L) {
-                qv = *reinterpret_cast<const uint4 *>(Q + (int64_t)t * a.stok + c);
-                av = *reinterpret_cast<const uint4 *>(dA + (int64_t)t * a.H * D + c);
+        const E *O = (const E *)a.out + base;
+        const E *dO = (const E *)a.dout + base;
+        const E *G = a.g ? (const E *)a.g + base : nullptr;
+        E *dG = a.dg ? (E *)a.dg + base : nullptr;
+        E *dAw = (E *)a.da + rh * (int64_t)L * D;
+        for (int idx = tid; idx < LP * CPT; idx += NT) {
+            const int t = idx / CPT, c = (idx % CPT) * VEC;
+            const bool valid = t < L;
+            uint4 qv = make_uint4(0, 0, 0, 0), ov = qv, dov = qv, gv = qv;
+            if (valid) {
+                const int64_t off = (int64_t)t * a.stok + c;
+                qv = *reinterpret_cast<const uint4 *>(Q + off);
+                ov = *reinterpret_cast<const uint4 *>(O + off);
+                dov = *reinterpret_cast<const uint4 *>(dO + off);
+                if (G) gv = *reinterpret_cast<const uint4 *>(G + off);
             }
+            const E *oe = reinterpret_cast<const E *>(&ov);
+            const E *de = reinterpret_cast<const E *>(&dov);
+            const E *ge = reinterpret_cast<const E *>(&gv);
+            uint4 dav, dgv;
+            E *dae = reinterpret_cast<E *>(&dav);
+            E *dge = reinterpret_cast<E *>(&dgv);
+            float part = 0.0f;
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) {
+                const float o = Tr<T>::to_f(oe[e]), d = Tr<T>::to_f(de[e]);
+                part = __builtin_fmaf(d, o, part);
+                if (G) {
+                    const float sg = 1.0f / (1.0f + __builtin_amdgcn_exp2f(-Tr<T>::to_f(ge[e]) * kLog2e));
+                    dae[e] = Tr<T>::from_f(d * sg);
+                    dge[e] = Tr<T>::from_f(d * o * (1.0f - sg));
+                } else {
+                    dae[e] = de[e];
+                }
+            }
+            // Dsum of the token: sum over its CPT consecutive lanes
+#pragma unroll
+            for (int off = 1; off < CPT; off <<= 1) part += __shfl_xor(part, off);
+            if (valid) {
+                if (dG) *reinterpret_cast<uint4 *>(dG + (int64_t)t * a.stok + c) = dgv;
+                *reinterpret_cast<uint4 *>(dAw + (int64_t)t * D + c) = dav;
+                if (c == 0) a.dsum[rh * L + t] = part;
+            }
+            if (c == 0) dsum_lds[t] = valid ? part : 0.0f;
             *reinterpret_cast<uint4 *>(&q_lds[t * RSTR + c]) = qv;
-            *reinterpret_cast<uint4 *>(&da_lds[t * RSTR + c]) = av;
+            *reinterpret_cast<uint4 *>(&da_lds[t * RSTR + c]) = dav;
             const E *qe = reinterpret_cast<const E *>(&qv);
-            const E *ae = reinterpret_cast<const E *>(&av);
 #pragma unroll
             for (int e = 0; e < VEC; ++e) {
                 qt_lds[(c + e) * TSTR + t] = qe[e];
-                dat_lds[(c + e) * TSTR + t] = ae[e];
+                dat_lds[(c + e) * TSTR + t] = dae[e];
             }
         }
         for (int t = tid; t < LP; t += NT) {
-            float l2 = INFINITY, ds = 0.0f;  // padded or fully masked queries: P = 0
+            float l2 = INFINITY;  // padded or fully masked queries: P = 0
             if (t < L) {
-                const float l = a.lse[(r * a.H + hh) * a.L + t];
+                const float l = a.lse[rh * L + t];
                 if (l != -INFINITY) l2 = l * kLog2e;
-                ds = a.dsum[(r * a.H + hh) * a.L + t];
             }
             lse2_lds[t] = l2;
-            dsum_lds[t] = ds;
         }
+    }
 
-        // ---- this wave's key tile: K and V as B operands, K^T as A operand of dQ
-        const bool kin = key < L;
-        bool kvalid = kin;
-        if (kvalid && a.mask) kvalid = a.mask[r * a.L + key] != 0;
-        const bool kfull = __ballot(kvalid) == ~0ull;
-        const E *K = (const E *)a.k + base;
-        const E *V = (const E *)a.v + base;
-        ChFrag<T, D> kb, vb;
-        if (kin) {
-            kb.load(K + (int64_t)key * a.stok, h2);
-            vb.load(V + (int64_t)key * a.stok, h2);
+    // ---- this wave's key tile: K and V as B operands (lane = key)
+    const int kt = wave;
+    const int key = kt * 32 + n;
+    const int arow = sig(n);  // permuted A-operand row of this lane
+    const bool kin = key < L;
+    bool kvalid = kin;
+    if (kvalid && a.mask) kvalid = a.mask[r * a.L + key] != 0;
+    const bool kfull = __ballot(kvalid) == ~0ull;
+    ChFrag<T, D> kb, vb;
+    if (kin) {
+        kb.load((const E *)a.k + base + (int64_t)key * a.stok, h2);
+        vb.load((const E *)a.v + base + (int64_t)key * a.stok, h2);
+    } else {
+        kb.zero();
+        vb.zero();
+    }
+    const E *brow = a.biasT ? (const E *)a.biasT + ((b * a.H + hh) * (int64_t)L + (kin ? key : 0)) * L : nullptr;
+    const bool bias_vec = (L % VEC) == 0;
+    __syncthreads();
+
+    f32x16 dv_acc = zero16(), dk_acc = zero16();
+    const int nqt = (L + 31) / 32;
+#pragma unroll
+    for (int qt = 0; qt < NKT; ++qt) {
+        if (qt >= nqt) break;
+        // S = Q K^T and dP = dA V^T for 32 queries x this wave's 32 keys;
+        // lane = key, reg i = query qt*32 + krow(i, h2)
+        ChFrag<T, D> qa, daa;
+        qa.load(&q_lds[(qt * 32 + arow) * RSTR], h2);
+        daa.load(&da_lds[(qt * 32 + arow) * RSTR], h2);
+        f32x16 S = zero16(), dP = zero16();
+        ChFrag<T, D>::mma(S, qa, kb);
+        ChFrag<T, D>::mma(dP, daa, vb);
+        float bv[16];
+        if (brow && kin) {
+            load_row8<T>(brow, qt * 32 + 8 * h2, L, bias_vec, bv);
+            load_row8<T>(brow, qt * 32 + 16 + 8 * h2, L, bias_vec, bv + 8);
         } else {
-            kb.zero();
-            vb.zero();
-        }
-        K32 kT;  // kT rows: channel sig(n); k-slots: keys of the tile
-        if constexpr (sizeof(E) == 2) {
 #pragma unroll
-            for (int s = 0; s < 8; ++s) {
-                const int j0 = kt * 32 + 8 * h2 + s, j1 = kt * 32 + 16 + 8 * h2 + s;
-                uint16_t x0 = 0, x1 = 0;
-                if (krow_sig < D && j0 < L) x0 = K[(int64_t)j0 * a.stok + krow_sig];
-                if (krow_sig < D && j1 < L) x1 = K[(int64_t)j1 * a.stok + krow_sig];
-                kT.v[0][s] = __builtin_bit_cast(__bf16, x0);
-                kT.v[1][s] = __builtin_bit_cast(__bf16, x1);
-            }
+            for (int i = 0; i < 16; ++i) bv[i] = 0.0f;
+        }
+        float l2[16], dsv[16];
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            const int q0 = qt * 32 + 16 * half + 8 * h2;
+            const float4 *lp = reinterpret_cast<const float4 *>(&lse2_lds[q0]);
+            const float4 *dp = reinterpret_cast<const float4 *>(&dsum_lds[q0]);
+            const float4 x0 = lp[0], x1 = lp[1], y0 = dp[0], y1 = dp[1];
+            l2[8 * half + 0] = x0.x; l2[8 * half + 1] = x0.y; l2[8 * half + 2] = x0.z; l2[8 * half + 3] = x0.w;
+            l2[8 * half + 4] = x1.x; l2[8 * half + 5] = x1.y; l2[8 * half + 6] = x1.z; l2[8 * half + 7] = x1.w;
+            dsv[8 * half + 0] = y0.x; dsv[8 * half + 1] = y0.y; dsv[8 * half + 2] = y0.z; dsv[8 * half + 3] = y0.w;
+            dsv[8 * half + 4] = y1.x; dsv[8 * half + 5] = y1.y; dsv[8 * half + 6] = y1.z; dsv[8 * half + 7] = y1.w;
+        }
+        f32x16 P, dS;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const float t = __builtin_fmaf(S[i], a.scale, bv[i]);
+            float p = __builtin_amdgcn_exp2f(__builtin_fmaf(t, kLog2e, -l2[i]));
+            if (!kfull && !kvalid) p = 0.0f;
+            P[i] = p;
+            dS[i] = p * (dP[i] - dsv[i]);
+        }
+        const K32 pb = Tr<T>::pack(P);
+        const K32 dsb = Tr<T>::pack(dS);
+        // dV^T += dA^T P ;  dK^T += Q^T dS   (A rows: channel sig(n))
+        K32 dat, qtf;
+        if (arow < D) {
+            dat = load_k32<T>(&dat_lds[arow * TSTR + qt * 32], h2);
+            qtf = load_k32<T>(&qt_lds[arow * TSTR + qt * 32], h2);
         } else {
-#pragma unroll
-            for (int u = 0; u < 16; ++u) {
-                const int j = kt * 32 + krow(u, h2);
-                kT.v[u] = (krow_sig < D && j < L) ? K[(int64_t)j * a.stok + krow_sig] : 0.0f;
-            }
+            dat = zero_k32<T>();
+            qtf = zero_k32<T>();
         }
-        __syncthreads();
+        Tr<T>::mma_k32(dv_acc, dat, pb);
+        Tr<T>::mma_k32(dk_acc, qtf, dsb);
+    }
 
-        f32x16 dv_acc = zero16(), dk_acc = zero16();
-        E *my_dsc = dsc + wave * 32 * SSTR;
-        const int nqt = (L + 31) / 32;
+    // ---- dK and dV of this key tile are complete (lane = key, reg = channel)
+    if (kin) {
+        E *dKp = (E *)a.dk + base + (int64_t)key * a.stok;
+        E *dVp = (E *)a.dv + base + (int64_t)key * a.stok;
 #pragma unroll
-        for (int qt = 0; qt < NKT; ++qt) {
-            if (qt >= nqt) break;
-            // S = Q K^T and dP = dA V^T for (32 queries x this wave's 32 keys);
-            // lane = key, reg i = query krow(i, h2)
-            ChFrag<T, D> qa, daa;
-            qa.load(&q_lds[(qt * 32 + krow_sig) * RSTR], h2);
-            daa.load(&da_lds[(qt * 32 + krow_sig) * RSTR], h2);
-            f32x16 S = zero16(), dP = zero16();
-            ChFrag<T, D>::mma(S, qa, kb);
-            ChFrag<T, D>::mma(dP, daa, vb);
-            float l2[16], dsv[16];
+        for (int half = 0; half < 2; ++half) {
+            const int c0 = 16 * half + 8 * h2;
+            if (c0 >= D) continue;
+            const int o = 8 * half;
+            if constexpr (sizeof(E) == 2) {
+                uint4 wk, wv;
+                uint32_t *pk = reinterpret_cast<uint32_t *>(&wk), *pv = reinterpret_cast<uint32_t *>(&wv);
 #pragma unroll
-            for (int half = 0; half < 2; ++half) {
-                const int q0 = qt * 32 + 16 * half + 8 * h2;
-                const float4 *lp = reinterpret_cast<const float4 *>(&lse2_lds[q0]);
-                const float4 *dp = reinterpret_cast<const float4 *>(&dsum_lds[q0]);
-                float4 x0 = lp[0], x1 = lp[1], y0 = dp[0], y1 = dp[1];
-                l2[8 * half + 0] = x0.x; l2[8 * half + 1] = x0.y; l2[8 * half + 2] = x0.z; l2[8 * half + 3] = x0.w;
-                l2[8 * half + 4] = x1.x; l2[8 * half + 5] = x1.y; l2[8 * half + 6] = x1.z; l2[8 * half + 7] = x1.w;
-                dsv[8 * half + 0] = y0.x; dsv[8 * half + 1] = y0.y; dsv[8 * half + 2] = y0.z; dsv[8 * half + 3] = y0.w;
-                dsv[8 * half + 4] = y1.x; dsv[8 * half + 5] = y1.y; dsv[8 * half + 6] = y1.z; dsv[8 * half + 7] = y1.w;
-            }
-            f32x16 P, dS;
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int qi = qt * 32 + krow(i, h2);
-                float bv = 0.0f;
-                if (bias_plane && kin && qi < L) bv = Tr<T>::to_f(bias_plane[(int64_t)qi * L + key]);
-                const float t = __builtin_fmaf(S[i], a.scale, bv);
-                float p = __builtin_amdgcn_exp2f(__builtin_fmaf(t, kLog2e, -l2[i]));
-                if (!kfull && !kvalid) p = 0.0f;
-                P[i] = p;
-                dS[i] = p * (dP[i] - dsv[i]);
-            }
-            const K32 pb = Tr<T>::pack(P);
-            const K32 dsb = Tr<T>::pack(dS);
-            // dV^T += dA^T P ;  dK^T += Q^T dS   (A rows: channel sig(n))
-            K32 dat, qtf;
-            if (krow_sig < D) {
-                dat = load_k32<T>(&dat_lds[krow_sig * TSTR + qt * 32], h2);
-                qtf = load_k32<T>(&qt_lds[krow_sig * TSTR + qt * 32], h2);
-            } else {
-                dat = zero_k32<T>();
-                qtf = zero_k32<T>();
-            }
-            Tr<T>::mma_k32(dv_acc, dat, pb);
-            Tr<T>::mma_k32(dk_acc, qtf, dsb);
-            // dQ^T (channels x queries) = K^T dS^T: dS goes through LDS to
-            // swap its lane/register roles
-#pragma unroll
-            for (int i = 0; i < 16; ++i) my_dsc[krow(i, h2) * SSTR + n] = Tr<T>::from_f(dS[i]);
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-            const K32 dst = load_k32<T>(&my_dsc[n * SSTR], h2);
-            f32x16 dq = zero16();
-            Tr<T>::mma_k32(dq, kT, dst);
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int ch = krow(i, h2);
-                if (ch < D) atomicAdd(&dq_acc[(qt * 32 + n) * QSTR + ch], dq[i]);
-            }
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        }
-
-        // ---- dK and dV of this key tile are complete
-        if (kin) {
-            E *dKp = (E *)a.dk + base + (int64_t)key * a.stok;
-            E *dVp = (E *)a.dv + base + (int64_t)key * a.stok;
-#pragma unroll
-            for (int half = 0; half < 2; ++half) {
-                const int c0 = 16 * half + 8 * h2;
-                if (c0 >= D) continue;
-                if constexpr (sizeof(E) == 2) {
-                    uint4 wk, wv;
-                    uint32_t *pk = reinterpret_cast<uint32_t *>(&wk), *pv = reinterpret_cast<uint32_t *>(&wv);
-#pragma unroll
-                    for (int s = 0; s < 4; ++s) {
-                        pk[s] = (uint32_t)f2bf(dk_acc[8 * half + 2 * s] * a.scale) |
-                                ((uint32_t)f2bf(dk_acc[8 * half + 2 * s + 1] * a.scale) << 16);
-                        pv[s] = (uint32_t)f2bf(dv_acc[8 * half + 2 * s]) |
-                                ((uint32_t)f2bf(dv_acc[8 * half + 2 * s + 1]) << 16);
-                    }
-                    *reinterpret_cast<uint4 *>(dKp + c0) = wk;
-                    *reinterpret_cast<uint4 *>(dVp + c0) = wv;
-                } else {
-                    const int o = 8 * half;
-                    *reinterpret_cast<float4 *>(dKp + c0) =
-                        make_float4(dk_acc[o] * a.scale, dk_acc[o + 1] * a.scale, dk_acc[o + 2] * a.scale, dk_acc[o + 3] * a.scale);
-                    *reinterpret_cast<float4 *>(dKp + c0 + 4) =
-                        make_float4(dk_acc[o + 4] * a.scale, dk_acc[o + 5] * a.scale, dk_acc[o + 6] * a.scale, dk_acc[o + 7] * a.scale);
-                    *reinterpret_cast<float4 *>(dVp + c0) = make_float4(dv_acc[o], dv_acc[o + 1], dv_acc[o + 2], dv_acc[o + 3]);
-                    *reinterpret_cast<float4 *>(dVp + c0 + 4) = make_float4(dv_acc[o + 4], dv_acc[o + 5], dv_acc[o + 6], dv_acc[o + 7]);
+                for (int s = 0; s < 4; ++s) {
+                    pk[s] = (uint32_t)f2bf(dk_acc[o + 2 * s] * a.scale) |
+                            ((uint32_t)f2bf(dk_acc[o + 2 * s + 1] * a.scale) << 16);
+                    pv[s] = (uint32_t)f2bf(dv_acc[o + 2 * s]) | ((uint32_t)f2bf(dv_acc[o + 2 * s + 1]) << 16);
                 }
+                *reinterpret_cast<uint4 *>(dKp + c0) = wk;
+                *reinterpret_cast<uint4 *>(dVp + c0) = wv;
+            } else {
+                *reinterpret_cast<float4 *>(dKp + c0) = make_float4(
+                    dk_acc[o] * a.scale, dk_acc[o + 1] * a.scale, dk_acc[o + 2] * a.scale, dk_acc[o + 3] * a.scale);
+                *reinterpret_cast<float4 *>(dKp + c0 + 4) = make_float4(
+                    dk_acc[o + 4] * a.scale, dk_acc[o + 5] * a.scale, dk_acc[o + 6] * a.scale, dk_acc[o + 7] * a.scale);
+                *reinterpret_cast<float4 *>(dVp + c0) = make_float4(dv_acc[o], dv_acc[o + 1], dv_acc[o + 2], dv_acc[o + 3]);
+                *reinterpret_cast<float4 *>(dVp + c0 + 4) =
+                    make_float4(dv_acc[o + 4], dv_acc[o + 5], dv_acc[o + 6], dv_acc[o + 7]);
             }
-        }
-        __syncthreads();  // every wave's dQ contributions are in dq_acc
-        E *dQ = (E *)a.dq + base;
-        for (int idx = tid; idx < L * D; idx += NT) {
-            const int t = idx / D, c = idx % D;
-            dQ[(int64_t)t * a.stok + c] = Tr<T>::from_f(dq_acc[t * QSTR + c] * a.scale);
         }
     }
 }
 
 // ---------------------------------------------------------------------------
-struct DbiasArgs {
+struct QbArgs {
     const void *q, *k, *v, *bias;
     const uint8_t *mask;
     const float *lse;
-    const void *da;
-    const float *dsum;
-    float *part;   // [B][H][chunks][L][L]
+    const void *da;      // workspace [N][H][L][D]
+    const float *dsum;   // workspace [N][H][L]
+    void *dq;
+    float *part;         // [B][H][chunks][L][L] or null
     int64_t L, rpb, srow, stok, chunks, rows_per_chunk;
     int H;
     float scale;
 };
 
-// One workgroup = (plane b, head h, key tile kt, chunk of rows).  Wave w owns
-// query tiles w, w+4, ...; lane = key, registers = queries (same D layout as
-// the main kernel), so the accumulator is NQW x 16 registers per lane.
 template <typename T, int D, int NKT>
-__global__ void __launch_bounds__(256) dbias_kernel(DbiasArgs a) {
+__global__ void __launch_bounds__(NKT * 64) qbias_kernel(QbArgs a) {
     using E = typename Tr<T>::elem;
-    constexpr int NQW = (NKT + 3) / 4;  // query tiles per wave
+    using K32 = typename Tr<T>::K32;
+    constexpr int VEC = Tr<T>::VEC;
+    constexpr int NT = NKT * 64;
+    constexpr int PSTR = D + 4;  // dQ partial stride in LDS (floats)
+    __shared__ __attribute__((aligned(16))) float dqp[NKT * 32 * PSTR];
+
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int h2 = lane >> 5, n = lane & 31;
     const int L = (int)a.L;
-    const int nkt = (L + 31) / 32;
-    // unit -> (b, chunk, kt, head), head fastest
+    const int nqt = (L + 31) / 32;
+    // unit -> (b, chunk, qt, head), head fastest
     const int64_t unit = xcd_unit(blockIdx.x, gridDim.x);
     const int hh = (int)(unit % a.H);
     int64_t rest = unit / a.H;
-    const int kt = (int)(rest % nkt);
-    rest /= nkt;
+    const int qt = (int)(rest % nqt);
+    rest /= nqt;
     const int64_t chunk = rest % a.chunks, b = rest / a.chunks;
     const int64_t r_begin = b * a.rpb + chunk * a.rows_per_chunk;
     int64_t r_end = r_begin + a.rows_per_chunk;
     if (r_end > (b + 1) * a.rpb) r_end = (b + 1) * a.rpb;
 
-    const int key = kt * 32 + n;
-    const bool kin = key < L;
-    const int krow_sig = sig(n);
-    const E *bias_plane = (const E *)a.bias + (b * a.H + hh) * (int64_t)L * L;
+    const int kt = wave;
+    const int qi = qt * 32 + n;  // this lane's query
+    const bool qvalid = qi < L;
+    const int arow = sig(n);     // permuted A-operand row (key of the tile / channel)
+    const int akey = kt * 32 + arow;
+    const bool vec_ok = (L % VEC) == 0;
 
-    // bias tile (constant over rows) and accumulators
-    float bt[NQW][16];
-    f32x16 acc[NQW];
+    // bias tile of (this query tile, this key tile): constant over rows
+    float bt[16];
+    if (a.bias && qvalid) {
+        const E *row = (const E *)a.bias + ((b * a.H + hh) * (int64_t)L + qi) * L;
+        load_row8<T>(row, kt * 32 + 8 * h2, L, vec_ok, bt);
+        load_row8<T>(row, kt * 32 + 16 + 8 * h2, L, vec_ok, bt + 8);
+    } else {
 #pragma unroll
-    for (int j = 0; j < NQW; ++j) {
-        acc[j] = zero16();
-        const int qt = wave + 4 * j;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const int qi = qt * 32 + krow(i, h2);
-            bt[j][i] = (kin && qi < L) ? Tr<T>::to_f(bias_plane[(int64_t)qi * L + key]) : 0.0f;
-        }
+        for (int i = 0; i < 16; ++i) bt[i] = 0.0f;
     }
+    f32x16 acc = zero16();
 
     for (int64_t r = r_begin; r < r_end; ++r) {
         const int64_t base = r * a.srow + (int64_t)hh * D;
-        bool kvalid = kin;
-        if (kvalid && a.mask) kvalid = a.mask[r * a.L + key] != 0;
-        if (__ballot(kvalid) == 0ull) continue;  // every key of the tile masked: dS = 0
-        const bool kfull = __ballot(kvalid) == ~0ull;
-        const E *K = (const E *)a.k + base;
-        const E *V = (const E *)a.v + base;
-        ChFrag<T, D> kb, vb;
-        if (kin) {
-            kb.load(K + (int64_t)key * a.stok, h2);
-            vb.load(V + (int64_t)key * a.stok, h2);
-        } else {
-            kb.zero();
-            vb.zero();
+        const int64_t rh = r * a.H + hh;
+        // keep bits of this wave's 32 keys (wave-uniform)
+        bool kk = false;
+        if (lane < 32) {
+            const int key = kt * 32 + lane;
+            kk = key < L && (!a.mask || a.mask[r * a.L + key] != 0);
         }
-        const E *Q = (const E *)a.q + base;
-        const E *dA = (const E *)a.da + ((r * L) * a.H + hh) * D;
-        const float *lse = a.lse + (r * a.H + hh) * a.L;
-        const float *dsum = a.dsum + (r * a.H + hh) * a.L;
-#pragma unroll
-        for (int j = 0; j < NQW; ++j) {
-            const int qt = wave + 4 * j;
-            if (qt * 32 >= L) break;
-            const int qrow = qt * 32 + krow_sig;  // A-operand row of this lane
-            ChFrag<T, D> qa, daa;
-            if (qrow < L) {
-                qa.load(Q + (int64_t)qrow * a.stok, h2);
-                daa.load(dA + (int64_t)qrow * a.H * D, h2);
+        const uint32_t kbits = (uint32_t)__ballot(kk);
+        f32x16 dq = zero16();
+        if (kbits != 0) {
+            const E *K = (const E *)a.k + base;
+            const E *V = (const E *)a.v + base;
+            ChFrag<T, D> qb, dab, ka, va;
+            if (qvalid) {
+                qb.load((const E *)a.q + base + (int64_t)qi * a.stok, h2);
+                dab.load((const E *)a.da + (rh * L + qi) * D, h2);
             } else {
-                qa.zero();
-                daa.zero();
+                qb.zero();
+                dab.zero();
             }
+            if (akey < L) {
+                ka.load(K + (int64_t)akey * a.stok, h2);
+                va.load(V + (int64_t)akey * a.stok, h2);
+            } else {
+                ka.zero();
+                va.zero();
+            }
+            // K^T as the A operand of dQ^T: rows = channel arow, k-slots = keys
+            K32 kT;
+            if constexpr (sizeof(E) == 2) {
+#pragma unroll
+                for (int s = 0; s < 8; ++s) {
+                    const int j0 = kt * 32 + 8 * h2 + s, j1 = kt * 32 + 16 + 8 * h2 + s;
+                    uint16_t x0 = 0, x1 = 0;
+                    if (arow < D && j0 < L) x0 = K[(int64_t)j0 * a.stok + arow];
+                    if (arow < D && j1 < L) x1 = K[(int64_t)j1 * a.stok + arow];
+                    kT.v[0][s] = __builtin_bit_cast(__bf16, x0);
+                    kT.v[1][s] = __builtin_bit_cast(__bf16, x1);
+                }
+            } else {
+#pragma unroll
+                for (int u = 0; u < 16; ++u) {
+                    const int j = kt * 32 + krow(u, h2);
+                    kT.v[u] = (arow < D && j < L) ? K[(int64_t)j * a.stok + arow] : 0.0f;
+                }
+            }
+            float l2 = INFINITY, ds = 0.0f;
+            if (qvalid) {
+                const float l = a.lse[rh * L + qi];
+                if (l != -INFINITY) l2 = l * kLog2e;
+                ds = a.dsum[rh * L + qi];
+            }
+            // S^T = K Q^T, dP^T = V dA^T: lane = query, reg i = key kt*32 + krow(i, h2)
             f32x16 S = zero16(), dP = zero16();
-            ChFrag<T, D>::mma(S, qa, kb);
-            ChFrag<T, D>::mma(dP, daa, vb);
+            ChFrag<T, D>::mma(S, ka, qb);
+            ChFrag<T, D>::mma(dP, va, dab);
+            const bool full = kbits == 0xffffffffu;
+            f32x16 dS;
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
-                const int qi = qt * 32 + krow(i, h2);
-                float l2 = INFINITY, ds = 0.0f;
-                if (qi < L) {
-                    const float l = lse[qi];
-                    if (l != -INFINITY) l2 = l * kLog2e;
-                    ds = dsum[qi];
-                }
-                const float t = __builtin_fmaf(S[i], a.scale, bt[j][i]);
+                const float t = __builtin_fmaf(S[i], a.scale, bt[i]);
                 float p = __builtin_amdgcn_exp2f(__builtin_fmaf(t, kLog2e, -l2));
-                if (!kfull && !kvalid) p = 0.0f;
-                acc[j][i] += p * (dP[i] - ds);
+                if (!full && !((kbits >> krow(i, h2)) & 1u)) p = 0.0f;
+                dS[i] = p * (dP[i] - ds);
+                acc[i] += dS[i];
+            }
+            // dQ^T (channels x queries) = K^T dS^T over this wave's keys
+            Tr<T>::mma_k32(dq, kT, Tr<T>::pack(dS));
+        }
+        // fixed-order sum of the waves' dQ partials through LDS
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            const int c0 = 16 * half + 8 * h2;
+            if (c0 >= D) continue;
+            float *dst = &dqp[(wave * 32 + n) * PSTR + c0];
+            *reinterpret_cast<float4 *>(dst) = make_float4(dq[8 * half], dq[8 * half + 1], dq[8 * half + 2], dq[8 * half + 3]);
+            *reinterpret_cast<float4 *>(dst + 4) =
+                make_float4(dq[8 * half + 4], dq[8 * half + 5], dq[8 * half + 6], dq[8 * half + 7]);
+        }
+        __syncthreads();
+        for (int idx = tid; idx < 32 * D; idx += NT) {
+            const int q = idx / D, c = idx % D;
+            if (qt * 32 + q < L) {
+                float s = 0.0f;
+#pragma unroll
+                for (int w = 0; w < NKT; ++w) s += dqp[(w * 32 + q) * PSTR + c];
+                ((E *)a.dq)[base + (int64_t)(qt * 32 + q) * a.stok + c] = Tr<T>::from_f(s * a.scale);
             }
         }
+        __syncthreads();
     }
 
-    if (kin) {
-        float *pp = a.part + ((b * a.H + hh) * a.chunks + chunk) * (int64_t)L * L;
+    // ---- partial dBias tile of this chunk: [qi][kt*32 + krow(i, h2)]
+    if (a.part && qvalid) {
+        float *pp = a.part + (((b * a.H + hh) * a.chunks + chunk) * (int64_t)L + qi) * L;
 #pragma unroll
-        for (int j = 0; j < NQW; ++j) {
-            const int qt = wave + 4 * j;
+        for (int half = 0; half < 2; ++half) {
+            const int j0 = kt * 32 + 16 * half + 8 * h2;
+            if (j0 + 8 <= L && (L % 4) == 0) {
+                *reinterpret_cast<float4 *>(pp + j0) = make_float4(acc[8 * half], acc[8 * half + 1], acc[8 * half + 2], acc[8 * half + 3]);
+                *reinterpret_cast<float4 *>(pp + j0 + 4) =
+                    make_float4(acc[8 * half + 4], acc[8 * half + 5], acc[8 * half + 6], acc[8 * half + 7]);
+            } else {
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int qi = qt * 32 + krow(i, h2);
-                if (qi < L) pp[(int64_t)qi * L + key] = acc[j][i];
+                for (int s = 0; s < 8; ++s)
+                    if (j0 + s < L) pp[j0 + s] = acc[8 * half + s];
             }
         }
     }
@@ -463,77 +491,59 @@ __global__ void __launch_bounds__(256) dbias_reduce_kernel(const float *__restri
 }
 
 // ---------------------------------------------------------------------------
-template <typename T, int D>
-hipError_t launch_prep(const Problem &p, const PrepArgs &pa, hipStream_t s) {
-    const int64_t total = p.N * p.L * p.H;
-    const int64_t blocks = (total + 255) / 256;
-    hipLaunchKernelGGL((prep_kernel<T, D>), dim3((unsigned)blocks), dim3(256), 0, s, pa);
-    return hipGetLastError();
-}
-
 template <typename T, int D, int NKT>
-hipError_t launch_main_dbias(const Problem &p, const MainArgs &ma, const DbiasArgs &da, const BwdPlan &plan,
-                             hipStream_t s) {
-    hipLaunchKernelGGL((main_kernel<T, D, NKT>), dim3((unsigned)(p.N * p.H)), dim3(NKT * 64), 0, s, ma);
+hipError_t launch_passes(const Problem &p, const KvArgs &ka, const QbArgs &qa, const BwdPlan &plan, hipStream_t s) {
+    hipLaunchKernelGGL((kv_kernel<T, D, NKT>), dim3((unsigned)(p.N * p.H)), dim3(NKT * 64), 0, s, ka);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || !da.bias) return e;
-    hipLaunchKernelGGL((dbias_kernel<T, D, NKT>), dim3((unsigned)plan.n_wg), dim3(256), 0, s, da);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((qbias_kernel<T, D, NKT>), dim3((unsigned)plan.n_wg), dim3(NKT * 64), 0, s, qa);
     return hipGetLastError();
 }
 
 template <typename T, int D>
-hipError_t launch_main_d(const Problem &p, const MainArgs &ma, const DbiasArgs &da, const BwdPlan &plan,
-                         hipStream_t s) {
+hipError_t launch_passes_d(const Problem &p, const KvArgs &ka, const QbArgs &qa, const BwdPlan &plan, hipStream_t s) {
     const int64_t nkt = (p.L + 31) / 32;
-    if (nkt <= 1) return launch_main_dbias<T, D, 1>(p, ma, da, plan, s);
-    if (nkt <= 2) return launch_main_dbias<T, D, 2>(p, ma, da, plan, s);
-    if (nkt <= 4) return launch_main_dbias<T, D, 4>(p, ma, da, plan, s);
-    if constexpr (sizeof(typename Tr<T>::elem) == 4 && D == 32) {
-        return hipErrorInvalidValue;  // rejected by the ABI layer before any launch
-    } else {
-        return launch_main_dbias<T, D, 8>(p, ma, da, plan, s);
-    }
+    if (nkt <= 1) return launch_passes<T, D, 1>(p, ka, qa, plan, s);
+    if (nkt <= 2) return launch_passes<T, D, 2>(p, ka, qa, plan, s);
+    if (nkt <= 4) return launch_passes<T, D, 4>(p, ka, qa, plan, s);
+    return launch_passes<T, D, 8>(p, ka, qa, plan, s);
 }
 
 template <typename T>
 hipError_t launch_bwd_t(const Problem &p, const BwdPtrs &x, void *ws, const BwdPlan &plan, hipStream_t s) {
+    using E = typename Tr<T>::elem;
     char *w = (char *)ws;
-    PrepArgs pa;
-    pa.out = x.out; pa.dout = x.dout; pa.g = x.g;
-    pa.da = w + plan.off_da;
-    pa.dsum = (float *)(w + plan.off_dsum);
-    pa.dg = x.dg;
-    pa.N = p.N; pa.L = p.L; pa.srow = p.srow; pa.stok = p.stok; pa.H = p.H;
+    const int64_t planes = x.bias ? (p.N / p.rpb) * p.H : 0;
     hipError_t e;
-    switch (p.D) {
-        case 8: e = launch_prep<T, 8>(p, pa, s); break;
-        case 16: e = launch_prep<T, 16>(p, pa, s); break;
-        default: e = launch_prep<T, 32>(p, pa, s); break;
+    if (x.bias) {
+        const int64_t tiles = (p.L + 31) / 32;
+        hipLaunchKernelGGL((transpose_kernel<E>), dim3((unsigned)(planes * tiles * tiles)), dim3(256), 0, s,
+                           (const E *)x.bias, (E *)(w + plan.off_biast), p.L, tiles);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
     }
-    if (e != hipSuccess) return e;
-
     const int64_t rpb = x.bias ? p.rpb : p.N;
     const float scale = 1.0f / sqrtf((float)p.D);
-    MainArgs ma;
-    ma.q = x.q; ma.k = x.k; ma.v = x.v; ma.bias = x.bias; ma.mask = x.mask; ma.lse = x.lse;
-    ma.da = pa.da; ma.dsum = pa.dsum;
-    ma.dq = x.dq; ma.dk = x.dk; ma.dv = x.dv;
-    ma.L = p.L; ma.rpb = rpb; ma.srow = p.srow; ma.stok = p.stok; ma.H = p.H; ma.scale = scale;
-    DbiasArgs da;
-    da.q = x.q; da.k = x.k; da.v = x.v; da.bias = x.bias; da.mask = x.mask; da.lse = x.lse;
-    da.da = pa.da; da.dsum = pa.dsum;
-    da.part = (float *)(w + plan.off_part);
-    da.L = p.L; da.rpb = rpb; da.srow = p.srow; da.stok = p.stok;
-    da.chunks = plan.chunks; da.rows_per_chunk = plan.rows_per_chunk;
-    da.H = p.H; da.scale = scale;
+    KvArgs ka;
+    ka.q = x.q; ka.k = x.k; ka.v = x.v; ka.g = x.g; ka.out = x.out; ka.dout = x.dout;
+    ka.biasT = x.bias ? (const void *)(w + plan.off_biast) : nullptr;
+    ka.mask = x.mask; ka.lse = x.lse;
+    ka.dk = x.dk; ka.dv = x.dv; ka.dg = x.dg;
+    ka.da = w + plan.off_da; ka.dsum = (float *)(w + plan.off_dsum);
+    ka.L = p.L; ka.rpb = rpb; ka.srow = p.srow; ka.stok = p.stok; ka.H = p.H; ka.scale = scale;
+    QbArgs qa;
+    qa.q = x.q; qa.k = x.k; qa.v = x.v; qa.bias = x.bias; qa.mask = x.mask; qa.lse = x.lse;
+    qa.da = ka.da; qa.dsum = ka.dsum; qa.dq = x.dq;
+    qa.part = x.bias ? (float *)(w + plan.off_part) : nullptr;
+    qa.L = p.L; qa.rpb = rpb; qa.srow = p.srow; qa.stok = p.stok;
+    qa.chunks = plan.chunks; qa.rows_per_chunk = plan.rows_per_chunk;
+    qa.H = p.H; qa.scale = scale;
     switch (p.D) {
-        case 8: e = launch_main_d<T, 8>(p, ma, da, plan, s); break;
-        case 16: e = launch_main_d<T, 16>(p, ma, da, plan, s); break;
-        default: e = launch_main_d<T, 32>(p, ma, da, plan, s); break;
+        case 8: e = launch_passes_d<T, 8>(p, ka, qa, plan, s); break;
+        case 16: e = launch_passes_d<T, 16>(p, ka, qa, plan, s); break;
+        default: e = launch_passes_d<T, 32>(p, ka, qa, plan, s); break;
     }
     if (e != hipSuccess || !x.bias) return e;
-
-    const int64_t planes = (p.N / p.rpb) * p.H;
     const int64_t pe = p.L * p.L;
     int64_t blocks = (planes * pe + 255) / 256;
     if (blocks > 8192) blocks = 8192;
@@ -547,30 +557,36 @@ hipError_t launch_bwd_t(const Problem &p, const BwdPtrs &x, void *ws, const BwdP
 BwdPlan plan_bwd(const Problem &p, bool has_bias) {
     BwdPlan pl;
     const int64_t es = p.dtype == 1 ? 2 : 4;
-    const int64_t planes = has_bias ? p.N / p.rpb : 0;
-    const int64_t nkt = (p.L + 31) / 32;
-    int64_t target = 1024;  // dbias workgroups (4 waves each) to fill 256 CUs
-    if (const char *env = getenv("EVO_ATTN_DBIAS_WG")) {
+    const int64_t planes = has_bias ? p.N / p.rpb : (p.N > 0 ? 1 : 0);
+    const int64_t rpb = has_bias ? p.rpb : p.N;
+    const int64_t nqt = (p.L + 31) / 32;
+    const int64_t waves = nqt <= 1 ? 1 : nqt <= 2 ? 2 : nqt <= 4 ? 4 : 8;  // per qbias workgroup
+    // qbias workgroups: enough waves to fill the chip (2048 = 8 per CU), with
+    // as few row chunks as that allows (each chunk costs one partial dBias plane)
+    int64_t target_waves = 2048;
+    if (const char *env = getenv("EVO_ATTN_QBIAS_WAVES")) {
         const long v = atol(env);
-        if (v > 0) target = v;
+        if (v > 0) target_waves = v;
     }
     int64_t chunks = 0, g = 1;
-    if (has_bias && p.rpb > 0 && nkt > 0) {
-        const int64_t base = planes * p.H * nkt;
-        chunks = (target + base - 1) / base;
+    if (planes > 0 && rpb > 0 && nqt > 0) {
+        const int64_t per_chunk = planes * p.H * nqt * waves;  // waves per row chunk
+        chunks = (target_waves + per_chunk - 1) / per_chunk;
         if (chunks < 1) chunks = 1;
-        if (chunks > p.rpb) chunks = p.rpb;
-        g = (p.rpb + chunks - 1) / chunks;
-        chunks = (p.rpb + g - 1) / g;
+        if (chunks > rpb) chunks = rpb;
+        g = (rpb + chunks - 1) / chunks;
+        chunks = (rpb + g - 1) / g;
     }
     pl.chunks = chunks;
     pl.rows_per_chunk = g;
-    pl.n_wg = planes * p.H * nkt * chunks;
+    pl.n_wg = planes * p.H * nqt * chunks;
     size_t off = 0;
     pl.off_da = off;
     off = align256(off + (size_t)(p.N * p.L * p.H * p.D * es));
     pl.off_dsum = off;
     off = align256(off + (size_t)(p.N * p.H * p.L) * 4);
+    pl.off_biast = off;
+    if (has_bias) off = align256(off + (size_t)(planes * p.H * p.L * p.L * es));
     pl.off_part = off;
     if (has_bias) off = align256(off + (size_t)(planes * p.H * chunks * p.L * p.L) * 4);
     pl.total = off;

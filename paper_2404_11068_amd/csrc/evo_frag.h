@@ -172,6 +172,45 @@ template <> struct ChFrag<bf16_t, 8> {
     }
 };
 
+// ---------------------------------------------------------------------------
+// k32 A operand of a contraction over 32 rows of a row-major bf16 LDS tile X
+// (X[row][col], `stride` elements per row), where the operand's row m is
+// column sig(m) of X and its k-slots are rows kbase + {8h+s, 16+8h+s}:
+//     A[m][k] = X[kbase + k][sig(m)]      (a transposed read of X)
+// Built from ds_read_b64_tr_b16: within each 16-lane group, output lane j
+// element e receives element j%4 of the 8-byte chunk addressed by source lane
+// 4e + j/4 of that group.  Source lane i of group G therefore addresses
+// row kbase + 16t + 8(G/2) + 4u + i/4, columns c0(i) .. c0(i)+3 with
+// c0 = 16(G%2) + 4*sig2(i%4) (sig2 swaps the two bits), for MFMA t and half u.
+// Columns >= ncols (head_dim) come out as zero.
+typedef short short4tr __attribute__((ext_vector_type(4)));
+typedef short short8tr __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ Tr<bf16_t>::K32 load_k32_tr(const uint16_t *X, int stride, int kbase, int ncols,
+                                                      int lane) {
+    const int G = lane >> 4, i = lane & 15;
+    const int q = i & 3;
+    int c0 = 16 * (G & 1) + 4 * (((q & 1) << 1) | (q >> 1));
+    const bool col_ok = c0 < ncols;
+    if (!col_ok) c0 = 0;  // keep the address inside the tile; the lanes fed by it are zeroed below
+    const int rbase = kbase + 8 * (G >> 1) + (i >> 2);
+    Tr<bf16_t>::K32 f;
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+        const uint16_t *src = X + (rbase + 16 * t) * stride + c0;
+        const short4tr lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) short4tr *)(src));
+        const short4tr hi =
+            __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) short4tr *)(src + 4 * stride));
+        // whole-vector concatenation: element-wise __bf16 insertion of these
+        // results was miscompiled (only the first dword of each read survived)
+        const short8tr both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        f.v[t] = __builtin_bit_cast(bf16x8, both);
+    }
+    // the operand row of this lane is channel sig(lane % 32)
+    if (sig(lane & 31) >= ncols) f = Tr<bf16_t>::K32{};
+    return f;
+}
+
 __device__ __forceinline__ f32x16 zero16() {
     f32x16 z;
 #pragma unroll

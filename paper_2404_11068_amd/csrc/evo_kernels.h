@@ -35,9 +35,9 @@ struct BwdPtrs {
 // Backward scratch plan: where each buffer lives inside the workspace.
 struct BwdPlan {
     int64_t chunks;          // row chunks per bias plane (dBias partial planes per plane and head)
-    int64_t rows_per_chunk;  // rows summed by one dbias workgroup
-    int64_t n_wg;            // workgroups of the dbias kernel
-    size_t off_da, off_dsum, off_part, total;
+    int64_t rows_per_chunk;  // rows handled by one qbias workgroup
+    int64_t n_wg;            // workgroups of the qbias kernel
+    size_t off_da, off_dsum, off_biast, off_part, total;
 };
 
 BwdPlan plan_bwd(const Problem &p, bool has_bias);

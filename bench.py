@@ -31,8 +31,37 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 MFMA
 MFMA_F32_PEAK_TFLOPS = 157.3
 
 
+def _align(x: int) -> int:
+    return (x + 255) // 256 * 256
+
+
+def kernel_model(w, es: int, ws_bytes: int):
+    """Per-launch algorithmic traffic (each input and output of the kernel
+    counted once, the shared bias plane once) and MFMA flops of every kernel
+    of one step, in launch order.  T = one [N, L, H, d] token tensor."""
+    N, L, H, d = w.n_rows, w.seq_len, w.n_heads, w.head_dim
+    T = N * L * H * d * es
+    lse = N * H * L * 4
+    B = N // w.rows_per_bias if w.bias else 0
+    bias = B * H * L * L * es
+    mask = N * L if w.mask != "none" else 0
+    g = 1 if w.gate else 0
+    S = N * H * L * L  # logits
+    parts = max(0, ws_bytes - _align(T) - _align(lse) - (_align(bias) if w.bias else 0))
+    ks = [("fwd_kernel", (3 + g) * T + bias + mask + T + lse, 4.0 * S * d)]
+    if w.bias:
+        ks.append(("bias_transpose", 2 * bias, 0.0))
+    # dK/dV pass: reads Q K V O dO [G] lse bias^T mask, writes dK dV dA [dG] Dsum
+    ks.append(("kv_kernel", (5 + g) * T + lse + bias + mask + (3 + g) * T + lse, 8.0 * S * d))
+    # dQ/dBias pass: reads Q K V dA lse Dsum bias mask, writes dQ and the partial dBias planes
+    ks.append(("qbias_kernel", 4 * T + 2 * lse + bias + mask + T + parts, 6.0 * S * d))
+    if w.bias:
+        ks.append(("dbias_reduce", parts + B * H * L * L * 4, 0.0))
+    return ks
+
+
 def algorithmic_bytes(w, es: int):
-    """Bytes each call must move at least once (bias counted once)."""
+    """Bytes the forward and the backward must move at least once."""
     tok = w.n_rows * w.seq_len * w.n_heads * w.head_dim * es
     lse = w.n_rows * w.n_heads * w.seq_len * 4
     bias = (w.n_rows // w.rows_per_bias) * w.n_heads * w.seq_len ** 2 * es if w.bias else 0
@@ -54,7 +83,11 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-baseline duration")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (reference for HBM byte counters)")
+    ap.add_argument("--source-hash", action="store_true", help="print the kernel-source hash and exit")
     args = ap.parse_args()
+    if args.source_hash:
+        print(kernel_source_hash())
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(rows shard across GPUs with no communication in the forward and one dBias "
@@ -96,48 +129,77 @@ def main():
     def fwd():
         ea.evo_attn_fwd(q, k, v, g, bias, mask, rows_per_bias=rpb, out=out, lse=lse, stream=stream)
 
-    def bwd():
+    def bwd(events=None):
         ea.evo_attn_bwd(q, k, v, g, bias, mask, out, lse, dout, rows_per_bias=rpb, dq=dq, dk=dk,
-                        dv=dv, dgate=dg, dbias=dbias, workspace=ws, stream=stream)
+                        dv=dv, dgate=dg, dbias=dbias, workspace=ws, stream=stream, events=events)
 
     for _ in range(args.warmup):
         fwd()
         bwd()
     torch.cuda.synchronize()
 
-    # timed region: K steps, events around every call on the launch stream
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
-           torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    start, stop = mk(), mk()
+
+    # timed region: K plain steps bracketed by events on the launch stream
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     start.record(stream)
-    for e0, e1, e2 in ev:
-        e0.record(stream)
+    for _ in range(args.steps):
         fwd()
-        e1.record(stream)
         bwd()
-        e2.record(stream)
     stop.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     total_ms = start.elapsed_time(stop)
     ms_step = total_ms / args.steps
-    fwd_ms = float(np.mean([a.elapsed_time(b) for a, b, _ in ev]))
-    bwd_ms = float(np.mean([b.elapsed_time(c) for _, b, c in ev]))
+
+    # per-kernel timing: K more steps with events on the launch stream around
+    # the forward kernel and (through evo_attn_bwd_traced) around every
+    # backward kernel; recording them adds a few microseconds per event, which
+    # is why the headline time above comes from plain steps
+    nk = ea.evo_attn_bwd_kernel_count(bias is not None)
+    fev = [(mk(), mk()) for _ in range(args.steps)]
+    bev = [[mk() for _ in range(nk + 1)] for _ in range(args.steps)]
+    for e in [x for p_ in fev for x in p_] + [x for l_ in bev for x in l_]:
+        e.record(stream)  # create the HIP events before timing
+    torch.cuda.synchronize()
+    for (e0, e1), evs in zip(fev, bev):
+        e0.record(stream)
+        fwd()
+        e1.record(stream)
+        bwd(evs)
+    torch.cuda.synchronize()
+    fwd_ms = float(np.mean([a.elapsed_time(b) for a, b in fev]))
+    bwd_ms = float(np.mean([l_[0].elapsed_time(l_[-1]) for l_ in bev]))
+    kern_ms = [fwd_ms] + [float(np.mean([l_[j].elapsed_time(l_[j + 1]) for l_ in bev])) for j in range(nk)]
 
     flops = w.flops_fwd() + w.flops_bwd()
     tflops = flops / (ms_step * 1e-3) / 1e12
     fwd_bytes, bwd_bytes = algorithmic_bytes(w, es)
-
-    # roofline of the forward kernel (one kernel per evo_attn_fwd call, so the
-    # event pair around the call brackets exactly that kernel)
-    fwd_gbs = fwd_bytes / (fwd_ms * 1e-3) / 1e9
-    roofline = {"kernel": "fwd_kernel", "bound": "hbm", "achieved": round(fwd_gbs, 1),
-                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(fwd_gbs / HBM_PEAK_GBS, 4),
-                "traffic": None, "avg_ms": round(fwd_ms, 5),
-                "algorithmic_bytes": fwd_bytes,
-                "mfma_tflops": round(w.flops_fwd() / (fwd_ms * 1e-3) / 1e12, 1)}
+    model = kernel_model(w, es, ws.numel())
+    assert len(model) == len(kern_ms), (len(model), len(kern_ms))
+    kernels = {}
+    for (name, nbytes, kflops), ms in zip(model, kern_ms):
+        kernels[name] = {"avg_ms": round(ms, 5), "algorithmic_bytes": int(nbytes),
+                         "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                         "mfma_tflops": round(kflops / (ms * 1e-3) / 1e12, 1)}
+    dom = max(range(len(model)), key=lambda i: kern_ms[i])
+    dname, dbytes, dflops = model[dom]
+    dms = kern_ms[dom]
+    peak_mfma = MFMA_BF16_PEAK_TFLOPS if w.dtype == "bf16" else MFMA_F32_PEAK_TFLOPS
+    ridge = peak_mfma * 1e12 / (HBM_PEAK_GBS * 1e9)          # flop per byte
+    if dflops / max(dbytes, 1) >= ridge:
+        ach = dflops / (dms * 1e-3) / 1e12
+        roofline = {"bound": "mfma", "achieved": round(ach, 2), "peak": peak_mfma, "unit": "TFLOP/s",
+                    "frac": round(ach / peak_mfma, 4)}
+    else:
+        ach = dbytes / (dms * 1e-3) / 1e9
+        roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(ach / HBM_PEAK_GBS, 4)}
+    roofline.update({"traffic": measured_traffic(dname, w.name), "kernel": dname, "avg_ms": round(dms, 5),
+                     "algorithmic_bytes": int(dbytes), "flops": dflops,
+                     "intensity_flop_per_byte": round(dflops / max(dbytes, 1), 1)})
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -151,7 +213,7 @@ def main():
         "config": {"workload": w.name, "n_rows": N, "seq_len": L, "n_heads": H, "head_dim": d,
                    "rows_per_bias": rpb, "bias": w.bias, "gate": w.gate, "mask": w.mask,
                    "parallelism": "single-gpu"},
-        "fwd_ms": round(fwd_ms, 5), "bwd_ms": round(bwd_ms, 5),
+        "fwd_ms": round(fwd_ms, 5), "bwd_ms": round(bwd_ms, 5), "kernels": kernels,
         "fwd_bwd_frac_of_mfma_peak": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
         "fwd_bwd_hbm_gbs": round((fwd_bytes + bwd_bytes) / (ms_step * 1e-3) / 1e9, 1),
         "wall_s": round(wall, 3),
@@ -159,6 +221,37 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(line))
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary
+    (profiles/traffic.json: FETCH_SIZE and WRITE_SIZE scaled by a plain copy
+    kernel's readings), or None when there is none for this kernel and
+    workload or the kernel sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as f:
+            entries = json.load(f)
+    except (OSError, ValueError):
+        return None
+    for e in entries.get("entries", []):
+        if e.get("kernel") == kernel and e.get("workload") == workload:
+            if e.get("source_sha256") != kernel_source_hash():
+                return None
+            return e.get("bytes_per_launch")
+    return None
+
+
+def kernel_source_hash() -> str:
+    """sha256 over the HIP sources and headers that define the kernels."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2404_11068_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".h", ".cpp")):
+            with open(os.path.join(csrc, name), "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()
 
 
 def copy_calibration(torch, mib: int, steps: int):

@@ -121,14 +121,34 @@ size_t evo_attn_bwd_workspace_size(const evo_attn_dims *dims);
  *   workspace, workspace_bytes : caller-owned device scratch of at least
  *              evo_attn_bwd_workspace_size(dims) bytes, 256-byte aligned;
  *              its contents on entry do not matter
- * Repeated calls give bitwise identical dk, dv, dgate and dbias (dbias is a
- * fixed-order two-step reduction).  dq is summed over key tiles with on-chip
- * float atomics, so its last bit may vary between calls.
+ * Every sum (over keys, queries and the rows of a bias plane) runs in a
+ * fixed order without atomics, so repeated calls give bitwise identical
+ * results.
  */
 int evo_attn_bwd(const evo_attn_dims *dims, const void *q, const void *k, const void *v,
                  const void *gate, const void *bias, const uint8_t *key_mask, const void *out,
                  const float *lse, const void *dout, void *dq, void *dk, void *dv, void *dgate,
                  float *dbias, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Profiling variant of evo_attn_bwd (identical arguments and results).  The
+ * caller passes n_events hipEvent_t handles it created; the library records
+ * events[0] on `stream` before its first kernel and events[i] right after its
+ * i-th kernel, so event pairs bracket single kernels.  Kernel order in this
+ * version: [pair-bias transpose], dK/dV pass, dQ/dBias pass, [dBias reduce]
+ * (bracketed entries only when bias != NULL).  n_events must be at least
+ * evo_attn_bwd_kernel_count(bias != NULL) + 1 and every handle non-NULL,
+ * else EVO_ERR_INVALID_ARG.  Meant for benchmarks; recording events costs a
+ * few microseconds per call.
+ */
+int evo_attn_bwd_traced(const evo_attn_dims *dims, const void *q, const void *k, const void *v,
+                        const void *gate, const void *bias, const uint8_t *key_mask,
+                        const void *out, const float *lse, const void *dout, void *dq, void *dk,
+                        void *dv, void *dgate, float *dbias, void *workspace,
+                        size_t workspace_bytes, void *const *events, int n_events, void *stream);
+
+/* Number of kernels one evo_attn_bwd call launches (has_bias: bias != NULL). */
+int evo_attn_bwd_kernel_count(int has_bias);
 
 /* Static, human-readable text for a status code (never NULL). */
 const char *evo_attn_strerror(int status);

@@ -91,10 +91,12 @@ size_t evo_attn_bwd_workspace_size(const evo_attn_dims *dims) {
     return evo::plan_bwd(p, bias_ok).total;
 }
 
-int evo_attn_bwd(const evo_attn_dims *dims, const void *q, const void *k, const void *v, const void *gate,
-                 const void *bias, const uint8_t *key_mask, const void *out, const float *lse, const void *dout,
-                 void *dq, void *dk, void *dv, void *dgate, float *dbias, void *workspace, size_t workspace_bytes,
-                 void *stream) {
+namespace {
+
+int bwd_impl(const evo_attn_dims *dims, const void *q, const void *k, const void *v, const void *gate,
+             const void *bias, const uint8_t *key_mask, const void *out, const float *lse, const void *dout,
+             void *dq, void *dk, void *dv, void *dgate, float *dbias, void *workspace, size_t workspace_bytes,
+             void *stream, evo::Tracer *tr) {
     evo::Problem p;
     int st = check_dims(dims, bias != nullptr, &p);
     if (st) return st;
@@ -110,9 +112,37 @@ int evo_attn_bwd(const evo_attn_dims *dims, const void *q, const void *k, const 
         return EVO_ERR_ALIGNMENT;
     const evo::BwdPlan plan = evo::plan_bwd(p, bias != nullptr);
     if (!workspace || workspace_bytes < plan.total || ((uintptr_t)workspace & 255u) != 0) return EVO_ERR_WORKSPACE;
+    if (tr && tr->n < evo::bwd_kernel_count(bias != nullptr) + 1) return EVO_ERR_INVALID_ARG;
+    if (tr)
+        for (int i = 0; i < tr->n; ++i)
+            if (!tr->ev[i]) return EVO_ERR_INVALID_ARG;
     evo::BwdPtrs x{q, k, v, gate, bias, key_mask, out, lse, dout, dq, dk, dv, dgate, dbias};
-    hipError_t e = evo::launch_bwd(p, x, workspace, plan, (hipStream_t)stream);
+    hipError_t e = evo::launch_bwd(p, x, workspace, plan, (hipStream_t)stream, tr);
     return e == hipSuccess ? EVO_OK : EVO_ERR_HIP;
+}
+
+}  // namespace
+
+int evo_attn_bwd(const evo_attn_dims *dims, const void *q, const void *k, const void *v, const void *gate,
+                 const void *bias, const uint8_t *key_mask, const void *out, const float *lse, const void *dout,
+                 void *dq, void *dk, void *dv, void *dgate, float *dbias, void *workspace, size_t workspace_bytes,
+                 void *stream) {
+    return bwd_impl(dims, q, k, v, gate, bias, key_mask, out, lse, dout, dq, dk, dv, dgate, dbias, workspace,
+                    workspace_bytes, stream, nullptr);
+}
+
+int evo_attn_bwd_kernel_count(int has_bias) { return evo::bwd_kernel_count(has_bias != 0); }
+
+int evo_attn_bwd_traced(const evo_attn_dims *dims, const void *q, const void *k, const void *v, const void *gate,
+                        const void *bias, const uint8_t *key_mask, const void *out, const float *lse,
+                        const void *dout, void *dq, void *dk, void *dv, void *dgate, float *dbias, void *workspace,
+                        size_t workspace_bytes, void *const *events, int n_events, void *stream) {
+    if (!events || n_events < 1) return EVO_ERR_INVALID_ARG;
+    evo::Tracer tr;
+    tr.ev = (hipEvent_t const *)events;
+    tr.n = n_events;
+    return bwd_impl(dims, q, k, v, gate, bias, key_mask, out, lse, dout, dq, dk, dv, dgate, dbias, workspace,
+                    workspace_bytes, stream, &tr);
 }
 
 }  // extern "C"

@@ -104,7 +104,7 @@ struct KvArgs {
 };
 
 template <typename T, int D, int NKT>
-__global__ void __launch_bounds__(NKT * 64, (NKT == 8 && sizeof(typename Tr<T>::elem) == 2) ? 4 : 2) kv_kernel(KvArgs a) {
+__global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
     using E = typename Tr<T>::elem;
     using K32 = typename Tr<T>::K32;
     constexpr int VEC = Tr<T>::VEC;
@@ -113,10 +113,13 @@ __global__ void __launch_bounds__(NKT * 64, (NKT == 8 && sizeof(typename Tr<T>::
     constexpr int NT = NKT * 64;
     constexpr int RSTR = D + VEC;    // row-major LDS stride
     constexpr int TSTR = LP + VEC;   // transposed LDS stride
+    // bf16: Q^T and dA^T fragments come from the transposing LDS read of the
+    // row-major tiles; fp32 keeps explicit transposed copies
+    constexpr bool kTr = sizeof(E) == 2;
     __shared__ __attribute__((aligned(16))) E q_lds[LP * RSTR];
     __shared__ __attribute__((aligned(16))) E da_lds[LP * RSTR];
-    __shared__ __attribute__((aligned(16))) E qt_lds[D * TSTR];
-    __shared__ __attribute__((aligned(16))) E dat_lds[D * TSTR];
+    __shared__ __attribute__((aligned(16))) E qt_lds[kTr ? 8 : D * TSTR];
+    __shared__ __attribute__((aligned(16))) E dat_lds[kTr ? 8 : D * TSTR];
     __shared__ __attribute__((aligned(16))) float lse2_lds[LP];
     __shared__ __attribute__((aligned(16))) float dsum_lds[LP];
 
@@ -161,7 +164,7 @@ __global__ void __launch_bounds__(NKT * 64, (NKT == 8 && sizeof(typename Tr<T>::
                 const float o = Tr<T>::to_f(oe[e]), d = Tr<T>::to_f(de[e]);
                 part = __builtin_fmaf(d, o, part);
                 if (G) {
-                    const float sg = 1.0f / (1.0f + __builtin_amdgcn_exp2f(-Tr<T>::to_f(ge[e]) * kLog2e));
+                    const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-Tr<T>::to_f(ge[e]) * kLog2e));
                     dae[e] = Tr<T>::from_f(d * sg);
                     dge[e] = Tr<T>::from_f(d * o * (1.0f - sg));
                 } else {
@@ -179,11 +182,13 @@ __global__ void __launch_bounds__(NKT * 64, (NKT == 8 && sizeof(typename Tr<T>::
             if (c == 0) dsum_lds[t] = valid ? part : 0.0f;
             *reinterpret_cast<uint4 *>(&q_lds[t * RSTR + c]) = qv;
             *reinterpret_cast<uint4 *>(&da_lds[t * RSTR + c]) = dav;
-            const E *qe = reinterpret_cast<const E *>(&qv);
+            if constexpr (!kTr) {
+                const E *qe = reinterpret_cast<const E *>(&qv);
 #pragma unroll
-            for (int e = 0; e < VEC; ++e) {
-                qt_lds[(c + e) * TSTR + t] = qe[e];
-                dat_lds[(c + e) * TSTR + t] = dae[e];
+                for (int e = 0; e < VEC; ++e) {
+                    qt_lds[(c + e) * TSTR + t] = qe[e];
+                    dat_lds[(c + e) * TSTR + t] = dae[e];
+                }
             }
         }
         for (int t = tid; t < LP; t += NT) {
@@ -230,12 +235,17 @@ __global__ void __launch_bounds__(NKT * 64, (NKT == 8 && sizeof(typename Tr<T>::
         ChFrag<T, D>::mma(S, qa, kb);
         ChFrag<T, D>::mma(dP, daa, vb);
         float bv[16];
-        if (brow && kin) {
-            load_row8<T>(brow, qt * 32 + 8 * h2, L, bias_vec, bv);
-            load_row8<T>(brow, qt * 32 + 16 + 8 * h2, L, bias_vec, bv + 8);
+        if (brow && bias_vec && (qt + 1) * 32 <= L && (kt + 1) * 32 <= L) {
+            // whole tile in range (uniform): two 16-byte loads of bias^T
+            load_row8<T>(brow, qt * 32 + 8 * h2, L, true, bv);
+            load_row8<T>(brow, qt * 32 + 16 + 8 * h2, L, true, bv + 8);
         } else {
 #pragma unroll
             for (int i = 0; i < 16; ++i) bv[i] = 0.0f;
+            if (brow && kin) {
+                load_row8<T>(brow, qt * 32 + 8 * h2, L, false, bv);
+                load_row8<T>(brow, qt * 32 + 16 + 8 * h2, L, false, bv + 8);
+            }
         }
         float l2[16], dsv[16];
 #pragma unroll
@@ -250,11 +260,11 @@ __global__ void __launch_bounds__(NKT * 64, (NKT == 8 && sizeof(typename Tr<T>::
             dsv[8 * half + 4] = y1.x; dsv[8 * half + 5] = y1.y; dsv[8 * half + 6] = y1.z; dsv[8 * half + 7] = y1.w;
         }
         f32x16 P, dS;
+        const float keepf = (kfull || kvalid) ? 1.0f : 0.0f;  // masked key: its lane's P is 0
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
             const float t = __builtin_fmaf(S[i], a.scale, bv[i]);
-            float p = __builtin_amdgcn_exp2f(__builtin_fmaf(t, kLog2e, -l2[i]));
-            if (!kfull && !kvalid) p = 0.0f;
+            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(t, kLog2e, -l2[i])) * keepf;
             P[i] = p;
             dS[i] = p * (dP[i] - dsv[i]);
         }
@@ -262,7 +272,10 @@ __global__ void __launch_bounds__(NKT * 64, (NKT == 8 && sizeof(typename Tr<T>::
         const K32 dsb = Tr<T>::pack(dS);
         // dV^T += dA^T P ;  dK^T += Q^T dS   (A rows: channel sig(n))
         K32 dat, qtf;
-        if (arow < D) {
+        if constexpr (kTr) {
+            dat = load_k32_tr(da_lds, RSTR, qt * 32, D, lane);
+            qtf = load_k32_tr(q_lds, RSTR, qt * 32, D, lane);
+        } else if (arow < D) {
             dat = load_k32<T>(&dat_lds[arow * TSTR + qt * 32], h2);
             qtf = load_k32<T>(&qt_lds[arow * TSTR + qt * 32], h2);
         } else {
@@ -324,9 +337,23 @@ template <typename T, int D, int NKT>
 __global__ void __launch_bounds__(NKT * 64) qbias_kernel(QbArgs a) {
     using E = typename Tr<T>::elem;
     using K32 = typename Tr<T>::K32;
+    constexpr bool kTr = sizeof(E) == 2;    // bf16: K^T fragments via the transposing LDS read
     constexpr int VEC = Tr<T>::VEC;
+    constexpr int CPT = D / VEC;            // 16-byte chunks per token
+    constexpr int LP = NKT * 32;
     constexpr int NT = NKT * 64;
-    constexpr int PSTR = D + 4;  // dQ partial stride in LDS (floats)
+    constexpr int KSTR = D + VEC;           // row stride of K, V, Q, dA tiles in LDS (elements)
+    constexpr int PSTR = D + 4;             // dQ partial stride in LDS (floats)
+    constexpr int NKV = (LP * CPT + NT - 1) / NT;  // 16-byte chunks of K (and of V) per thread
+    constexpr int NQC = (32 * CPT + NT - 1) / NT;  // 16-byte chunks of the Q (and dA) tile per thread
+    constexpr int NSUM = (32 * (D / 4) + NT - 1) / NT;  // 4-channel groups of dQ summed per thread
+    __shared__ __attribute__((aligned(16))) E k_lds[LP * KSTR];
+    __shared__ __attribute__((aligned(16))) E v_lds[LP * KSTR];
+    __shared__ __attribute__((aligned(16))) E q_lds[32 * KSTR];
+    __shared__ __attribute__((aligned(16))) E da_lds[32 * KSTR];
+    __shared__ __attribute__((aligned(16))) float lse2_lds[32];
+    __shared__ __attribute__((aligned(16))) float dsum_lds[32];
+    __shared__ uint32_t kbits_lds[NKT];
     __shared__ __attribute__((aligned(16))) float dqp[NKT * 32 * PSTR];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -347,94 +374,138 @@ __global__ void __launch_bounds__(NKT * 64) qbias_kernel(QbArgs a) {
     const int kt = wave;
     const int qi = qt * 32 + n;  // this lane's query
     const bool qvalid = qi < L;
-    const int arow = sig(n);     // permuted A-operand row (key of the tile / channel)
-    const int akey = kt * 32 + arow;
     const bool vec_ok = (L % VEC) == 0;
 
     // bias tile of (this query tile, this key tile): constant over rows
     float bt[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) bt[i] = 0.0f;
     if (a.bias && qvalid) {
         const E *row = (const E *)a.bias + ((b * a.H + hh) * (int64_t)L + qi) * L;
         load_row8<T>(row, kt * 32 + 8 * h2, L, vec_ok, bt);
         load_row8<T>(row, kt * 32 + 16 + 8 * h2, L, vec_ok, bt + 8);
-    } else {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) bt[i] = 0.0f;
     }
     f32x16 acc = zero16();
 
-    for (int64_t r = r_begin; r < r_end; ++r) {
+    // ---- one row's inputs, staged through registers (loads of row r+1 are in
+    // flight while row r is computed)
+    uint4 kpf[NKV], vpf[NKV], qpf[NQC], dapf[NQC];
+    float lpf = -INFINITY, dspf = 0.0f;
+    bool mpf = false;
+    auto prefetch = [&](int64_t r) {
         const int64_t base = r * a.srow + (int64_t)hh * D;
         const int64_t rh = r * a.H + hh;
-        // keep bits of this wave's 32 keys (wave-uniform)
-        bool kk = false;
-        if (lane < 32) {
-            const int key = kt * 32 + lane;
-            kk = key < L && (!a.mask || a.mask[r * a.L + key] != 0);
+#pragma unroll
+        for (int j = 0; j < NKV; ++j) {
+            const int idx = tid + j * NT;
+            const int t = idx / CPT, c = (idx % CPT) * VEC;
+            kpf[j] = make_uint4(0, 0, 0, 0);
+            vpf[j] = make_uint4(0, 0, 0, 0);
+            if (idx < LP * CPT && t < L) {
+                kpf[j] = *reinterpret_cast<const uint4 *>((const E *)a.k + base + (int64_t)t * a.stok + c);
+                vpf[j] = *reinterpret_cast<const uint4 *>((const E *)a.v + base + (int64_t)t * a.stok + c);
+            }
         }
-        const uint32_t kbits = (uint32_t)__ballot(kk);
+#pragma unroll
+        for (int j = 0; j < NQC; ++j) {
+            const int idx = tid + j * NT;
+            const int t = qt * 32 + idx / CPT, c = (idx % CPT) * VEC;
+            qpf[j] = make_uint4(0, 0, 0, 0);
+            dapf[j] = make_uint4(0, 0, 0, 0);
+            if (idx < 32 * CPT && t < L) {
+                qpf[j] = *reinterpret_cast<const uint4 *>((const E *)a.q + base + (int64_t)t * a.stok + c);
+                dapf[j] = *reinterpret_cast<const uint4 *>((const E *)a.da + (rh * L + t) * D + c);
+            }
+        }
+        if (tid < 32) {
+            const int t = qt * 32 + tid;
+            lpf = t < L ? a.lse[rh * L + t] : -INFINITY;
+            dspf = t < L ? a.dsum[rh * L + t] : 0.0f;
+        }
+        mpf = tid < L && (!a.mask || a.mask[r * a.L + tid] != 0);
+    };
+
+    if (r_begin < r_end) prefetch(r_begin);
+    for (int64_t r = r_begin; r < r_end; ++r) {
+        const int64_t base = r * a.srow + (int64_t)hh * D;
+        // ---- registers -> LDS
+#pragma unroll
+        for (int j = 0; j < NKV; ++j) {
+            const int idx = tid + j * NT;
+            if (idx < LP * CPT) {
+                const int t = idx / CPT, c = (idx % CPT) * VEC;
+                *reinterpret_cast<uint4 *>(&k_lds[t * KSTR + c]) = kpf[j];
+                *reinterpret_cast<uint4 *>(&v_lds[t * KSTR + c]) = vpf[j];
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < NQC; ++j) {
+            const int idx = tid + j * NT;
+            if (idx < 32 * CPT) {
+                const int t = idx / CPT, c = (idx % CPT) * VEC;
+                *reinterpret_cast<uint4 *>(&q_lds[t * KSTR + c]) = qpf[j];
+                *reinterpret_cast<uint4 *>(&da_lds[t * KSTR + c]) = dapf[j];
+            }
+        }
+        if (tid < 32) {
+            lse2_lds[tid] = (lpf == -INFINITY) ? INFINITY : lpf * kLog2e;  // fully masked query: P = 0
+            dsum_lds[tid] = dspf;
+        }
+        {
+            const unsigned long long bal = __ballot(mpf);  // NT >= LP: one key per thread
+            if (lane == 0) {
+                if (2 * wave < NKT) kbits_lds[2 * wave] = (uint32_t)bal;
+                if (2 * wave + 1 < NKT) kbits_lds[2 * wave + 1] = (uint32_t)(bal >> 32);
+            }
+        }
+        __syncthreads();
+        if (r + 1 < r_end) prefetch(r + 1);
+
+        const uint32_t kbits = __builtin_amdgcn_readfirstlane(kbits_lds[kt]);
         f32x16 dq = zero16();
         if (kbits != 0) {
-            const E *K = (const E *)a.k + base;
-            const E *V = (const E *)a.v + base;
             ChFrag<T, D> qb, dab, ka, va;
-            if (qvalid) {
-                qb.load((const E *)a.q + base + (int64_t)qi * a.stok, h2);
-                dab.load((const E *)a.da + (rh * L + qi) * D, h2);
-            } else {
-                qb.zero();
-                dab.zero();
-            }
-            if (akey < L) {
-                ka.load(K + (int64_t)akey * a.stok, h2);
-                va.load(V + (int64_t)akey * a.stok, h2);
-            } else {
-                ka.zero();
-                va.zero();
-            }
-            // K^T as the A operand of dQ^T: rows = channel arow, k-slots = keys
-            K32 kT;
-            if constexpr (sizeof(E) == 2) {
-#pragma unroll
-                for (int s = 0; s < 8; ++s) {
-                    const int j0 = kt * 32 + 8 * h2 + s, j1 = kt * 32 + 16 + 8 * h2 + s;
-                    uint16_t x0 = 0, x1 = 0;
-                    if (arow < D && j0 < L) x0 = K[(int64_t)j0 * a.stok + arow];
-                    if (arow < D && j1 < L) x1 = K[(int64_t)j1 * a.stok + arow];
-                    kT.v[0][s] = __builtin_bit_cast(__bf16, x0);
-                    kT.v[1][s] = __builtin_bit_cast(__bf16, x1);
-                }
-            } else {
-#pragma unroll
-                for (int u = 0; u < 16; ++u) {
-                    const int j = kt * 32 + krow(u, h2);
-                    kT.v[u] = (arow < D && j < L) ? K[(int64_t)j * a.stok + arow] : 0.0f;
-                }
-            }
-            float l2 = INFINITY, ds = 0.0f;
-            if (qvalid) {
-                const float l = a.lse[rh * L + qi];
-                if (l != -INFINITY) l2 = l * kLog2e;
-                ds = a.dsum[rh * L + qi];
-            }
+            qb.load(&q_lds[n * KSTR], h2);
+            dab.load(&da_lds[n * KSTR], h2);
+            ka.load(&k_lds[(kt * 32 + sig(n)) * KSTR], h2);
+            va.load(&v_lds[(kt * 32 + sig(n)) * KSTR], h2);
+            const float l2 = lse2_lds[n], ds = dsum_lds[n];
             // S^T = K Q^T, dP^T = V dA^T: lane = query, reg i = key kt*32 + krow(i, h2)
             f32x16 S = zero16(), dP = zero16();
             ChFrag<T, D>::mma(S, ka, qb);
             ChFrag<T, D>::mma(dP, va, dab);
-            const bool full = kbits == 0xffffffffu;
             f32x16 dS;
+            if (kbits == 0xffffffffu) {
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const float t = __builtin_fmaf(S[i], a.scale, bt[i]);
-                float p = __builtin_amdgcn_exp2f(__builtin_fmaf(t, kLog2e, -l2));
-                if (!full && !((kbits >> krow(i, h2)) & 1u)) p = 0.0f;
-                dS[i] = p * (dP[i] - ds);
-                acc[i] += dS[i];
+                for (int i = 0; i < 16; ++i) {
+                    const float t = __builtin_fmaf(S[i], a.scale, bt[i]);
+                    const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(t, kLog2e, -l2));
+                    dS[i] = p * (dP[i] - ds);
+                    acc[i] += dS[i];
+                }
+            } else {
+                const uint32_t kbl = kbits >> (8 * h2);
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const float t = __builtin_fmaf(S[i], a.scale, bt[i]);
+                    float p = __builtin_amdgcn_exp2f(__builtin_fmaf(t, kLog2e, -l2));
+                    p = ((kbl >> (16 * (i >> 3) + (i & 7))) & 1u) ? p : 0.0f;
+                    dS[i] = p * (dP[i] - ds);
+                    acc[i] += dS[i];
+                }
             }
             // dQ^T (channels x queries) = K^T dS^T over this wave's keys
+            K32 kT;
+            if constexpr (kTr) {
+                kT = load_k32_tr(k_lds, KSTR, kt * 32, D, lane);
+            } else {
+                const int c = sig(n);
+#pragma unroll
+                for (int u = 0; u < 16; ++u) kT.v[u] = c < D ? k_lds[(kt * 32 + krow(u, h2)) * KSTR + c] : 0.0f;
+            }
             Tr<T>::mma_k32(dq, kT, Tr<T>::pack(dS));
         }
-        // fixed-order sum of the waves' dQ partials through LDS
+        // ---- fixed-order sum of the waves' dQ partials through LDS
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
             const int c0 = 16 * half + 8 * h2;
@@ -445,16 +516,29 @@ __global__ void __launch_bounds__(NKT * 64) qbias_kernel(QbArgs a) {
                 make_float4(dq[8 * half + 4], dq[8 * half + 5], dq[8 * half + 6], dq[8 * half + 7]);
         }
         __syncthreads();
-        for (int idx = tid; idx < 32 * D; idx += NT) {
-            const int q = idx / D, c = idx % D;
-            if (qt * 32 + q < L) {
-                float s = 0.0f;
 #pragma unroll
-                for (int w = 0; w < NKT; ++w) s += dqp[(w * 32 + q) * PSTR + c];
-                ((E *)a.dq)[base + (int64_t)(qt * 32 + q) * a.stok + c] = Tr<T>::from_f(s * a.scale);
+        for (int j = 0; j < NSUM; ++j) {  // four consecutive channels per thread and step
+            const int idx = tid + j * NT;
+            if (idx >= 32 * (D / 4)) break;
+            const int q = idx / (D / 4), c = (idx % (D / 4)) * 4;
+            float4 s = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+#pragma unroll
+            for (int w = 0; w < NKT; ++w) {
+                const float4 x = *reinterpret_cast<const float4 *>(&dqp[(w * 32 + q) * PSTR + c]);
+                s.x += x.x; s.y += x.y; s.z += x.z; s.w += x.w;
+            }
+            if (qt * 32 + q < L) {
+                E *dst = (E *)a.dq + base + (int64_t)(qt * 32 + q) * a.stok + c;
+                if constexpr (sizeof(E) == 2) {
+                    uint2 w2;
+                    w2.x = (uint32_t)f2bf(s.x * a.scale) | ((uint32_t)f2bf(s.y * a.scale) << 16);
+                    w2.y = (uint32_t)f2bf(s.z * a.scale) | ((uint32_t)f2bf(s.w * a.scale) << 16);
+                    *reinterpret_cast<uint2 *>(dst) = w2;
+                } else {
+                    *reinterpret_cast<float4 *>(dst) = make_float4(s.x * a.scale, s.y * a.scale, s.z * a.scale, s.w * a.scale);
+                }
             }
         }
-        __syncthreads();
     }
 
     // ---- partial dBias tile of this chunk: [qi][kt*32 + krow(i, h2)]
@@ -492,35 +576,43 @@ __global__ void __launch_bounds__(256) dbias_reduce_kernel(const float *__restri
 
 // ---------------------------------------------------------------------------
 template <typename T, int D, int NKT>
-hipError_t launch_passes(const Problem &p, const KvArgs &ka, const QbArgs &qa, const BwdPlan &plan, hipStream_t s) {
+hipError_t launch_passes(const Problem &p, const KvArgs &ka, const QbArgs &qa, const BwdPlan &plan, hipStream_t s,
+                         Tracer &tr) {
     hipLaunchKernelGGL((kv_kernel<T, D, NKT>), dim3((unsigned)(p.N * p.H)), dim3(NKT * 64), 0, s, ka);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    tr.mark(s);
     hipLaunchKernelGGL((qbias_kernel<T, D, NKT>), dim3((unsigned)plan.n_wg), dim3(NKT * 64), 0, s, qa);
-    return hipGetLastError();
+    e = hipGetLastError();
+    if (e == hipSuccess) tr.mark(s);
+    return e;
 }
 
 template <typename T, int D>
-hipError_t launch_passes_d(const Problem &p, const KvArgs &ka, const QbArgs &qa, const BwdPlan &plan, hipStream_t s) {
+hipError_t launch_passes_d(const Problem &p, const KvArgs &ka, const QbArgs &qa, const BwdPlan &plan, hipStream_t s,
+                           Tracer &tr) {
     const int64_t nkt = (p.L + 31) / 32;
-    if (nkt <= 1) return launch_passes<T, D, 1>(p, ka, qa, plan, s);
-    if (nkt <= 2) return launch_passes<T, D, 2>(p, ka, qa, plan, s);
-    if (nkt <= 4) return launch_passes<T, D, 4>(p, ka, qa, plan, s);
-    return launch_passes<T, D, 8>(p, ka, qa, plan, s);
+    if (nkt <= 1) return launch_passes<T, D, 1>(p, ka, qa, plan, s, tr);
+    if (nkt <= 2) return launch_passes<T, D, 2>(p, ka, qa, plan, s, tr);
+    if (nkt <= 4) return launch_passes<T, D, 4>(p, ka, qa, plan, s, tr);
+    return launch_passes<T, D, 8>(p, ka, qa, plan, s, tr);
 }
 
 template <typename T>
-hipError_t launch_bwd_t(const Problem &p, const BwdPtrs &x, void *ws, const BwdPlan &plan, hipStream_t s) {
+hipError_t launch_bwd_t(const Problem &p, const BwdPtrs &x, void *ws, const BwdPlan &plan, hipStream_t s,
+                        Tracer &tr) {
     using E = typename Tr<T>::elem;
     char *w = (char *)ws;
     const int64_t planes = x.bias ? (p.N / p.rpb) * p.H : 0;
     hipError_t e;
+    tr.mark(s);
     if (x.bias) {
         const int64_t tiles = (p.L + 31) / 32;
         hipLaunchKernelGGL((transpose_kernel<E>), dim3((unsigned)(planes * tiles * tiles)), dim3(256), 0, s,
                            (const E *)x.bias, (E *)(w + plan.off_biast), p.L, tiles);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
+        tr.mark(s);
     }
     const int64_t rpb = x.bias ? p.rpb : p.N;
     const float scale = 1.0f / sqrtf((float)p.D);
@@ -539,9 +631,9 @@ hipError_t launch_bwd_t(const Problem &p, const BwdPtrs &x, void *ws, const BwdP
     qa.chunks = plan.chunks; qa.rows_per_chunk = plan.rows_per_chunk;
     qa.H = p.H; qa.scale = scale;
     switch (p.D) {
-        case 8: e = launch_passes_d<T, 8>(p, ka, qa, plan, s); break;
-        case 16: e = launch_passes_d<T, 16>(p, ka, qa, plan, s); break;
-        default: e = launch_passes_d<T, 32>(p, ka, qa, plan, s); break;
+        case 8: e = launch_passes_d<T, 8>(p, ka, qa, plan, s, tr); break;
+        case 16: e = launch_passes_d<T, 16>(p, ka, qa, plan, s, tr); break;
+        default: e = launch_passes_d<T, 32>(p, ka, qa, plan, s, tr); break;
     }
     if (e != hipSuccess || !x.bias) return e;
     const int64_t pe = p.L * p.L;
@@ -549,7 +641,9 @@ hipError_t launch_bwd_t(const Problem &p, const BwdPtrs &x, void *ws, const BwdP
     if (blocks > 8192) blocks = 8192;
     hipLaunchKernelGGL(dbias_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, s,
                        (const float *)(w + plan.off_part), x.dbias, planes, plan.chunks, pe);
-    return hipGetLastError();
+    e = hipGetLastError();
+    if (e == hipSuccess) tr.mark(s);
+    return e;
 }
 
 }  // namespace
@@ -593,9 +687,14 @@ BwdPlan plan_bwd(const Problem &p, bool has_bias) {
     return pl;
 }
 
-hipError_t launch_bwd(const Problem &p, const BwdPtrs &x, void *ws, const BwdPlan &plan, hipStream_t s) {
-    if (p.dtype == 1) return launch_bwd_t<bf16_t>(p, x, ws, plan, s);
-    return launch_bwd_t<float>(p, x, ws, plan, s);
+int bwd_kernel_count(bool has_bias) { return has_bias ? 4 : 2; }
+
+hipError_t launch_bwd(const Problem &p, const BwdPtrs &x, void *ws, const BwdPlan &plan, hipStream_t s,
+                      Tracer *tr) {
+    Tracer none;
+    Tracer &t = tr ? *tr : none;
+    if (p.dtype == 1) return launch_bwd_t<bf16_t>(p, x, ws, plan, s, t);
+    return launch_bwd_t<float>(p, x, ws, plan, s, t);
 }
 
 }  // namespace evo

@@ -251,7 +251,7 @@ __global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
 
         // ---- epilogue: normalise, gate, store O and lse
         if (qvalid) {
-            const float inv = lsum > 0.0f ? 1.0f / lsum : 0.0f;
+            const float inv = lsum > 0.0f ? __builtin_amdgcn_rcpf(lsum) : 0.0f;
             const int64_t tok = base + (int64_t)qi * a.stok;
             const E *G = a.g ? (const E *)a.g + tok : nullptr;
             E *O = (E *)a.out + tok;
@@ -266,7 +266,7 @@ __global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
                     float gv[8];
                     load8_vec<T>(G, cb, gv);
 #pragma unroll
-                    for (int s8 = 0; s8 < 8; ++s8) val[s8] = val[s8] / (1.0f + __builtin_amdgcn_exp2f(-gv[s8] * kLog2e));
+                    for (int s8 = 0; s8 < 8; ++s8) val[s8] *= __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-gv[s8] * kLog2e));
                 }
                 if constexpr (sizeof(E) == 2) {
                     uint4 w;

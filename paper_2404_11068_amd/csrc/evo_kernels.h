@@ -42,8 +42,22 @@ struct BwdPlan {
 
 BwdPlan plan_bwd(const Problem &p, bool has_bias);
 
+// Optional stage markers: records caller-owned events on the launch stream
+// before the first kernel and after each kernel (profiling only).
+struct Tracer {
+    hipEvent_t const *ev = nullptr;
+    int n = 0, next = 0;
+    void mark(hipStream_t s) {
+        if (ev && next < n) (void)hipEventRecord(ev[next], s);
+        ++next;
+    }
+};
+
+// kernels launched by one backward call (for Tracer sizing)
+int bwd_kernel_count(bool has_bias);
+
 hipError_t launch_fwd(const Problem &p, const FwdPtrs &x, hipStream_t s);
 hipError_t launch_bwd(const Problem &p, const BwdPtrs &x, void *ws, const BwdPlan &plan,
-                      hipStream_t s);
+                      hipStream_t s, Tracer *tr = nullptr);
 
 }  // namespace evo

@@ -65,6 +65,11 @@ def load_library():
         lib.evo_attn_bwd_workspace_size.restype = ctypes.c_size_t
         lib.evo_attn_bwd.argtypes = [D] + [P] * 15 + [ctypes.c_size_t, P]
         lib.evo_attn_bwd.restype = ctypes.c_int
+        lib.evo_attn_bwd_traced.argtypes = [D] + [P] * 15 + [ctypes.c_size_t, ctypes.POINTER(P),
+                                                            ctypes.c_int, P]
+        lib.evo_attn_bwd_traced.restype = ctypes.c_int
+        lib.evo_attn_bwd_kernel_count.argtypes = [ctypes.c_int]
+        lib.evo_attn_bwd_kernel_count.restype = ctypes.c_int
         lib.evo_attn_strerror.argtypes = [ctypes.c_int]
         lib.evo_attn_strerror.restype = ctypes.c_char_p
         lib.evo_attn_version.restype = ctypes.c_int
@@ -145,9 +150,18 @@ def evo_attn_bwd_workspace_size(q: torch.Tensor, rows_per_bias=None) -> int:
     return int(load_library().evo_attn_bwd_workspace_size(ctypes.byref(dims)))
 
 
+def evo_attn_bwd_kernel_count(has_bias: bool) -> int:
+    return int(load_library().evo_attn_bwd_kernel_count(1 if has_bias else 0))
+
+
 def evo_attn_bwd(q, k, v, gate, bias, key_mask, out, lse, dout, *, rows_per_bias=None,
-                 dq=None, dk=None, dv=None, dgate=None, dbias=None, workspace=None, stream=None):
-    """Backward pass; returns (dq, dk, dv, dgate or None, dbias or None)."""
+                 dq=None, dk=None, dv=None, dgate=None, dbias=None, workspace=None, stream=None,
+                 events=None):
+    """Backward pass; returns (dq, dk, dv, dgate or None, dbias or None).
+
+    With `events` (a list of torch.cuda.Event(enable_timing=True), at least
+    evo_attn_bwd_kernel_count(bias is not None) + 1 of them) the call goes to
+    evo_attn_bwd_traced, which records them around each of its kernels."""
     lib = load_library()
     _same_layout(q, k, v, gate, out, dout)
     dims = make_dims(q, rows_per_bias)
@@ -167,11 +181,19 @@ def evo_attn_bwd(q, k, v, gate, bias, key_mask, out, lse, dout, *, rows_per_bias
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
     key_mask = _mask_u8(key_mask)
-    st = lib.evo_attn_bwd(ctypes.byref(dims), _ptr(q), _ptr(k), _ptr(v), _ptr(gate), _ptr(bias),
-                          _ptr(key_mask), _ptr(out), _ptr(lse), _ptr(dout), _ptr(dq), _ptr(dk),
-                          _ptr(dv), _ptr(dgate), _ptr(dbias), _ptr(workspace),
-                          ctypes.c_size_t(workspace.numel() * workspace.element_size()),
-                          _stream(stream))
+    args = [ctypes.byref(dims), _ptr(q), _ptr(k), _ptr(v), _ptr(gate), _ptr(bias), _ptr(key_mask),
+            _ptr(out), _ptr(lse), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dgate), _ptr(dbias),
+            _ptr(workspace), ctypes.c_size_t(workspace.numel() * workspace.element_size())]
+    if events is None:
+        st = lib.evo_attn_bwd(*args, _stream(stream))
+        where = "evo_attn_bwd"
+    else:
+        for e in events:  # torch creates the HIP event lazily, on its first record
+            if not e.cuda_event:
+                e.record(torch.cuda.current_stream() if stream is None else stream)
+        handles = (ctypes.c_void_p * len(events))(*[ctypes.c_void_p(e.cuda_event) for e in events])
+        st = lib.evo_attn_bwd_traced(*args, handles, len(events), _stream(stream))
+        where = "evo_attn_bwd_traced"
     if st:
-        raise EvoAttnError(st, "evo_attn_bwd")
+        raise EvoAttnError(st, where)
     return dq, dk, dv, dgate, dbias

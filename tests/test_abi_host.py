@@ -27,6 +27,7 @@ def test_exports_every_declared_symbol():
     decls = re.findall(r"^\s*(?:int|size_t|const char \*)\s*(evo_attn_\w+)\s*\(",
                        open(HEADER).read(), flags=re.M)
     assert set(decls) == {"evo_attn_fwd", "evo_attn_bwd", "evo_attn_bwd_workspace_size",
+                          "evo_attn_bwd_traced", "evo_attn_bwd_kernel_count",
                           "evo_attn_strerror", "evo_attn_version"}
     for name in decls:
         assert hasattr(lib, name), name
@@ -114,6 +115,22 @@ def test_bwd_rejects_invalid_calls():
     assert _bwd(d, ws=FAKE + (1 << 20) + 16) == 4          # workspace not 256-byte aligned
     assert _bwd(d, dv=FAKE + 8 * 4096 + 8) == 3
     assert _bwd(_dims(seq_len=300)) == 2
+
+
+def test_traced_backward_validates_events():
+    lib = _lib()
+    d = _dims()
+    P = ctypes.c_void_p
+    n = lib.evo_attn_bwd_kernel_count(0)
+    assert n >= 1 and lib.evo_attn_bwd_kernel_count(1) >= n
+    args = [ctypes.byref(d)] + [P(FAKE + i * 4096) for i in range(3)] + [None, None, None] + \
+           [P(FAKE + i * 4096) for i in range(3, 9)] + [None, None, P(FAKE + (1 << 20)),
+                                                        ctypes.c_size_t(1 << 40)]
+    few = (P * n)(*[P(FAKE)] * n)                     # one event short
+    assert lib.evo_attn_bwd_traced(*args, few, n, None) == 1
+    nulls = (P * (n + 1))()                          # NULL handles
+    assert lib.evo_attn_bwd_traced(*args, nulls, n + 1, None) == 1
+    assert lib.evo_attn_bwd_traced(*args, None, 0, None) == 1
 
 
 def test_workspace_size_is_positive_and_monotone():

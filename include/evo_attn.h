@@ -82,7 +82,9 @@ typedef struct evo_attn_dims {
     int64_t seq_len;       /* L >= 0: queries == keys */
     int64_t rows_per_bias; /* >= 1; N % rows_per_bias == 0; ignored when bias is NULL */
     int64_t stride_row;    /* elements between rows r and r+1 of every token tensor */
-    int64_t stride_tok;    /* elements between tokens t and t+1; >= H*d */
+    int64_t stride_tok;    /* elements between tokens t and t+1; >= H*d;
+                              seq_len * stride_tok * element size must stay
+                              below 2^31 bytes (else EVO_ERR_UNSUPPORTED) */
 } evo_attn_dims;
 
 /*

@@ -36,6 +36,8 @@ int check_dims(const evo_attn_dims *d, bool has_bias, evo::Problem *p) {
     if ((int64_t)d->n_rows * d->seq_len * d->n_heads / 256 > 0x7fffffffLL) return EVO_ERR_UNSUPPORTED;
     const int es = d->dtype == EVO_DTYPE_BF16 ? 2 : 4;
     if ((d->stride_tok * es) % 16 != 0 || (d->stride_row * es) % 16 != 0) return EVO_ERR_ALIGNMENT;
+    // the kernels address the tokens of one row with 32-bit byte offsets
+    if ((int64_t)d->seq_len * d->stride_tok * es >= 0x7fffffffLL) return EVO_ERR_UNSUPPORTED;
     p->dtype = d->dtype;
     p->H = d->n_heads;
     p->D = d->head_dim;

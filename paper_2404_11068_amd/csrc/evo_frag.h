@@ -30,6 +30,46 @@ typedef short short4v __attribute__((ext_vector_type(4)));
 
 struct bf16_t { uint16_t bits; };   // storage type of the bf16 path
 
+// ---------------------------------------------------------------------------
+// Buffer-resource memory access.  A resource covers [base, base + bytes);
+// a load at an offset past the end reads zeros and a store there is dropped
+// by the hardware, so out-of-range lanes need no branch: every vector-memory
+// instruction is issued unconditionally, which keeps the compiler's in-order
+// load counters exact across software-pipelined loads.
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+// Note: __builtin_bit_cast applied to a vector COMPONENT (x.y, x[1]) reads
+// component 0 with this compiler; bit-cast whole vectors, then take
+// components of the result.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr uint32_t kOOB = 0x80000000u;  // past every resource (sizes stay below 2^31)
+
+__device__ __forceinline__ rsrc_t make_buf(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ u32x4 bload16(rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+__device__ __forceinline__ u32x2 bload8(rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+}
+__device__ __forceinline__ uint32_t bload4(rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+}
+__device__ __forceinline__ uint16_t bload2(rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
+}
+__device__ __forceinline__ uint8_t bload1(rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b8(r, off, 0, 0);
+}
+__device__ __forceinline__ void bstore16(u32x4 v, rsrc_t r, uint32_t off) {
+    __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, 0);
+}
+__device__ __forceinline__ void bstore4(uint32_t v, rsrc_t r, uint32_t off) {
+    __builtin_amdgcn_raw_buffer_store_b32(v, r, off, 0, 0);
+}
+
 __device__ __forceinline__ int sig(int m) { return (m & ~0xC) | ((m & 4) << 1) | ((m & 8) >> 1); }
 __device__ __forceinline__ int krow(int i, int h) { return 16 * (i >> 3) + 8 * h + (i & 7); }
 
@@ -122,6 +162,14 @@ template <typename T, int D> struct ChFrag;
 // fp32: D/2 MFMAs of k=2; lane half h holds channels h*D/2 + u, u < D/2
 template <int D> struct ChFrag<float, D> {
     float v[D / 2];
+    // tok = byte offset of the token's D channels in resource r
+    __device__ __forceinline__ void load(rsrc_t r, uint32_t tok, int h) {
+#pragma unroll
+        for (int u = 0; u < D / 2; u += 4) {
+            const f32x4 x = __builtin_bit_cast(f32x4, bload16(r, tok + (uint32_t)(h * (D / 2) + u) * 4u));
+            v[u] = x.x; v[u + 1] = x.y; v[u + 2] = x.z; v[u + 3] = x.w;
+        }
+    }
     __device__ __forceinline__ void load(const float *tok, int h) {
 #pragma unroll
         for (int u = 0; u < D / 2; u += 4) {
@@ -143,6 +191,11 @@ template <int D> struct ChFrag<float, D> {
 template <int D> struct ChFrag<bf16_t, D> {
     static_assert(D % 16 == 0, "bf16 head_dim 16/32 use k=16 MFMAs");
     bf16x8 v[D / 16];
+    __device__ __forceinline__ void load(rsrc_t r, uint32_t tok, int h) {
+#pragma unroll
+        for (int kk = 0; kk < D / 16; ++kk)
+            v[kk] = __builtin_bit_cast(bf16x8, bload16(r, tok + (uint32_t)(16 * kk + 8 * h) * 2u));
+    }
     __device__ __forceinline__ void load(const uint16_t *tok, int h) {
 #pragma unroll
         for (int kk = 0; kk < D / 16; ++kk) v[kk] = *reinterpret_cast<const bf16x8 *>(tok + 16 * kk + 8 * h);
@@ -163,6 +216,9 @@ template <int D> struct ChFrag<bf16_t, D> {
 // bf16, D = 8: one MFMA of k=8; lane half h holds channels 4h + s, s < 4
 template <> struct ChFrag<bf16_t, 8> {
     short4v v;
+    __device__ __forceinline__ void load(rsrc_t r, uint32_t tok, int h) {
+        v = __builtin_bit_cast(short4v, bload8(r, tok + (uint32_t)(4 * h) * 2u));
+    }
     __device__ __forceinline__ void load(const uint16_t *tok, int h) {
         v = *reinterpret_cast<const short4v *>(tok + 4 * h);
     }
@@ -187,7 +243,7 @@ typedef short short4tr __attribute__((ext_vector_type(4)));
 typedef short short8tr __attribute__((ext_vector_type(8)));
 
 __device__ __forceinline__ Tr<bf16_t>::K32 load_k32_tr(const uint16_t *X, int stride, int kbase, int ncols,
-                                                      int lane) {
+                                                      int lane, bool ones_row = false) {
     const int G = lane >> 4, i = lane & 15;
     const int q = i & 3;
     int c0 = 16 * (G & 1) + 4 * (((q & 1) << 1) | (q >> 1));
@@ -206,9 +262,41 @@ __device__ __forceinline__ Tr<bf16_t>::K32 load_k32_tr(const uint16_t *X, int st
         const short8tr both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
         f.v[t] = __builtin_bit_cast(bf16x8, both);
     }
-    // the operand row of this lane is channel sig(lane % 32)
-    if (sig(lane & 31) >= ncols) f = Tr<bf16_t>::K32{};
+    // the operand row of this lane is channel sig(lane % 32); with ones_row,
+    // channel ncols (< 32) is all ones, so the product also yields column sums
+    const int ch = sig(lane & 31);
+    if (ch >= ncols) {
+        const short v = (ones_row && ch == ncols) ? (short)0x3F80 : (short)0;
+        const short8tr w = {v, v, v, v, v, v, v, v};
+        f.v[0] = __builtin_bit_cast(bf16x8, w);
+        f.v[1] = __builtin_bit_cast(bf16x8, w);
+    }
     return f;
+}
+
+// ---------------------------------------------------------------------------
+// Constant A operand "c times a permuted identity" for the k32 contraction:
+// A[m][k] = c where k-slot k holds row sig(m) of the tile, else 0.  With a B
+// operand holding X[k][n] (k = key row of the tile, n = query), the product
+// adds c * X[sig(m)][n] to the D layout whose register i holds row krow(i, h)
+// -- i.e. it adds c times a [query][key] tile (read along keys) to logits
+// produced with sig-permuted key rows.  Used to fold the pair bias into the
+// MFMA accumulator.
+__device__ __forceinline__ Tr<bf16_t>::K32 diag_k32(float c, int lane) {
+    const int r = sig(lane & 31), h = lane >> 5;
+    Tr<bf16_t>::K32 f;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int s = 0; s < 8; ++s) f.v[t][s] = (__bf16)((r == 16 * t + 8 * h + s) ? c : 0.0f);
+    return f;
+}
+
+// sqrt(d) as a sum of two bf16 values (hi + lo matches sqrt(d) to ~3e-7)
+__device__ __forceinline__ void sqrt_split(int d, float &hi, float &lo) {
+    const float r = sqrtf((float)d);
+    hi = (float)(__bf16)r;
+    lo = (float)(__bf16)(r - hi);
 }
 
 __device__ __forceinline__ f32x16 zero16() {

@@ -4,20 +4,35 @@
 // per-query log-sum-exp (ScaleFold Section 3.3, "Multi Head Attention": the
 // pair bias enters the logits before the softmax; all of MHA in one kernel).
 //
-// Work unit = one (row, head).  A workgroup has one wave per 32-query tile
-// (seq_len <= 256, so at most 8 waves) and is persistent: it walks a strided
-// list of units, and while it computes one unit the global loads of the next
-// unit's K, V, Q and key mask are already in flight into registers.  K and V
-// sit row-major in LDS; the V^T operand of O^T = V^T P^T comes out of the
-// transposing LDS read (ds_read_b64_tr_b16) on the bf16 path.
+// Work unit = one (row, head), one workgroup per unit, one wave per
+// 32-query tile (seq_len <= 256, so at most 8 waves).  The kernel keeps its
+// registers low (about 90 at head_dim 32) so that two workgroups share a CU
+// and each hides the other's loads and barriers.  K and V sit row-major in
+// LDS; the V^T operand of O^T = V^T P^T comes out of the transposing LDS read
+// (ds_read_b64_tr_b16) on the bf16 path.
 //
 // Logits are produced transposed (S^T = K Q^T): a lane owns one query and
 // the keys sit in its registers, so row max and row sum are in-lane
 // reductions plus one exchange between the two lane halves, and the
 // probabilities in registers are already the B operand of O^T = V^T P^T.
-// A wave keeps the logits of 128 keys (4 tiles) in registers at a time,
-// takes their max and exponentials in two passes over registers, and
-// rescales its running sums between such chunks (once at seq_len 256).
+//
+// bf16 path, per key tile of 32 keys:
+//   * the logits are kept "raw", S_raw = K Q^T + sqrt(d) * bias; the pair
+//     bias enters through the MFMA accumulator: a constant A operand holding
+//     sqrt(d) (split into two bf16 terms) on a permuted diagonal times the
+//     bias row loaded as raw bf16 (the B operand) -- no per-logit unpacking;
+//   * the scale 1/sqrt(d) and log2(e) are folded into the exponent's FMA;
+//   * with head_dim < 32, a row of ones in the V^T operand makes the same
+//     MFMA produce the row sums of the probabilities.
+// The running max is only raised when a tile's max exceeds it by more than
+// 2^8 in the base-2 exponent, so rescaling the accumulators is rare.
+//
+// Memory: every global access is a buffer instruction on a per-unit
+// resource; out-of-range lanes get an out-of-range offset (zeros on load,
+// dropped on store) instead of a branch.  All loads are therefore issued
+// unconditionally, in the order they are needed (the next key tile's bias
+// before the current tile's math), which keeps the compiler's in-order load
+// counters exact.
 #include <math.h>
 
 #include "evo_frag.h"
@@ -28,6 +43,12 @@ namespace evo {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.69314718055994531f;
+
+// Running-max policy: the reference max is raised only where a chunk max
+// exceeds it by more than 2^kTau (base-2 exponent units), so unnormalised
+// probabilities stay below 2^kTau.
+constexpr float kTau = 8.0f;
 
 struct FwdArgs {
     const void *q, *k, *v, *g, *bias;
@@ -39,279 +60,333 @@ struct FwdArgs {
     float scale;
 };
 
-// 8 consecutive values row[j0 .. j0+7] as fp32 (vector load); caller
-// guarantees j0 + 8 <= n and 16-byte alignment
-template <typename T>
-__device__ __forceinline__ void load8_vec(const typename Tr<T>::elem *row, int j0, float *out8) {
-    using E = typename Tr<T>::elem;
-    if constexpr (sizeof(E) == 2) {
-        uint4 u = *reinterpret_cast<const uint4 *>(row + j0);
-        uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            out8[2 * s] = __builtin_bit_cast(float, w[s] << 16);
-            out8[2 * s + 1] = __builtin_bit_cast(float, w[s] & 0xffff0000u);
-        }
+// raw bf16 pair bias of key tile kt for query row qi, as the B operand of the
+// bias MFMA: k-slots {8h+s, 16+8h+s} = keys kt*32 + those slots.  Rows past L
+// read zeros; keys past L read the next row's values (those keys are masked,
+// so the values never matter).  BV: L % 8 == 0, rows are 16-byte aligned.
+template <bool BV>
+__device__ __forceinline__ Tr<bf16_t>::K32 bias_k32(rsrc_t rb, int qi, int kt, int L, int h) {
+    Tr<bf16_t>::K32 f;
+    const uint32_t e0 = (uint32_t)(qi * L + kt * 32 + 8 * h);  // element index of slot 0
+    if constexpr (BV) {
+        f.v[0] = __builtin_bit_cast(bf16x8, bload16(rb, e0 * 2u));
+        f.v[1] = __builtin_bit_cast(bf16x8, bload16(rb, e0 * 2u + 32u));
     } else {
-        float4 a = *reinterpret_cast<const float4 *>(row + j0);
-        float4 b = *reinterpret_cast<const float4 *>(row + j0 + 4);
-        out8[0] = a.x; out8[1] = a.y; out8[2] = a.z; out8[3] = a.w;
-        out8[4] = b.x; out8[5] = b.y; out8[6] = b.z; out8[7] = b.w;
-    }
-}
-
-template <typename T>
-__device__ __forceinline__ void load8_guarded(const typename Tr<T>::elem *row, int j0, int n, float *out8) {
+        short8tr w0, w1;
 #pragma unroll
-    for (int s = 0; s < 8; ++s) out8[s] = (j0 + s < n) ? Tr<T>::to_f(row[j0 + s]) : 0.0f;
+        for (int s = 0; s < 8; ++s) {
+            w0[s] = (short)bload2(rb, (e0 + s) * 2u);
+            w1[s] = (short)bload2(rb, (e0 + 16 + s) * 2u);
+        }
+        f.v[0] = __builtin_bit_cast(bf16x8, w0);
+        f.v[1] = __builtin_bit_cast(bf16x8, w1);
+    }
+    return f;
 }
 
-// unit index handled by workgroup slot `w` at step `it`: each XCD (blockIdx
-// % 8) walks its own contiguous share of the units, so the heads of one row
-// are processed at the same time on one XCD and share its L2.
-__device__ __forceinline__ int64_t unit_of(int64_t w, int64_t it, int64_t nwg, int64_t n_units) {
-    if (nwg % 8 != 0) return w + it * nwg;
-    const int64_t per_xcd = nwg / 8, x = w % 8, slot = w / 8;
-    const int64_t share = (n_units + 7) / 8;
-    const int64_t u = x * share + slot + it * per_xcd;
-    return (u < (x + 1) * share && u < n_units) ? u : n_units;  // n_units = past the end
+// 64-lane mask of the lanes whose logit register i belongs to a kept key:
+// register i of lane half h holds key krow(i, h) of the tile.
+__device__ __forceinline__ uint64_t key_lanes(uint32_t kb, int i) {
+    const uint64_t lo = (kb >> krow(i, 0)) & 1u, hi = (kb >> krow(i, 1)) & 1u;
+    return (lo ? 0x00000000ffffffffull : 0ull) | (hi ? 0xffffffff00000000ull : 0ull);
 }
 
-template <typename T, int D, int NKT>
+template <typename T, int D, int NKT, int KC, bool BV>
 __global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
     using E = typename Tr<T>::elem;
     using K32 = typename Tr<T>::K32;
-    constexpr bool kTr = sizeof(E) == 2;  // bf16: V^T fragments via the transposing LDS read
+    constexpr int ES = sizeof(E);
+    constexpr bool kBf = ES == 2;              // bf16: V^T via the transposing LDS read, bias via MFMA
+    constexpr bool kOnesRow = kBf && D < 32;   // row sums come out of the PV product
     constexpr int VEC = Tr<T>::VEC;
-    constexpr int CPT = D / VEC;          // 16-byte chunks per token
+    constexpr int CPT = D / VEC;               // 16-byte chunks per token
     constexpr int LP = NKT * 32;
     constexpr int NT = NKT * 64;
-    constexpr int KSTR = D + VEC;         // row stride of K / V in LDS (elements)
-    constexpr int VSTR = LP + VEC;        // row stride of V^T in LDS (fp32 path)
-    constexpr int KC = NKT < 4 ? NKT : 4; // key tiles per register-resident chunk
+    constexpr int KSTR = D + VEC;              // row stride of K / V in LDS (elements)
+    constexpr int VSTR = LP + VEC;             // row stride of V^T in LDS (fp32 path)
+    constexpr int NCH = NKT / KC;              // chunks of KC key tiles
     constexpr int NPF = (LP * CPT + NT - 1) / NT;  // 16-byte chunks of K (and of V) per thread
+    constexpr int NBB = kBf && BV ? KC : 1;    // bias fragments per chunk held in registers
+    constexpr int NG = ES == 2 ? 1 : 2;        // 16-byte gate loads per 8 channels
     __shared__ __attribute__((aligned(16))) E k_lds[LP * KSTR];
-    __shared__ __attribute__((aligned(16))) E v_lds[kTr ? LP * KSTR : D * VSTR];
+    __shared__ __attribute__((aligned(16))) E v_lds[kBf ? LP * KSTR : D * VSTR];
     __shared__ uint32_t kbits[NKT];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int h2 = lane >> 5, n = lane & 31;
     const int L = (int)a.L;
-    const int qt = wave;
-    const int qi = qt * 32 + n;
+    const int qi = wave * 32 + n;
     const bool qvalid = qi < L;
-    const bool bias_vec = (L % VEC) == 0;
-    const int64_t nwg = gridDim.x;
+    const bool has_bias = a.bias != nullptr, has_mask = a.mask != nullptr, has_gate = a.g != nullptr;
+    const uint32_t stok_b = (uint32_t)(a.stok * ES);
+    const uint32_t row_bytes = (uint32_t)(a.L * a.stok * ES);  // host: below 2^31
+    const uint32_t q_off = qvalid ? (uint32_t)qi * stok_b : kOOB;
 
-    // ---- prefetch registers for one unit
-    uint4 kpf[NPF], vpf[NPF];
-    ChFrag<T, D> qf;
-    bool mpf = false;
-    auto prefetch = [&](int64_t u) {
-        const int64_t r = u / a.H;
-        const int hh = (int)(u % a.H);
-        const int64_t base = r * a.srow + (int64_t)hh * D;
+    // one workgroup per (row, head) unit; consecutive units (the heads of a
+    // row) land on the same XCD
+    const int64_t u = xcd_unit(blockIdx.x, gridDim.x);
+    if (u >= a.n_units) return;
+    const int64_t r = u / a.H;
+    const int hh = (int)(u % a.H);
+    auto tok_buf = [&](const void *X) {
+        return make_buf((const E *)X + r * a.srow + (int64_t)hh * D, row_bytes);
+    };
+    const rsrc_t rb = has_bias ? make_buf((const E *)a.bias + ((r / a.rpb) * a.H + hh) * (int64_t)L * L,
+                                          (uint32_t)(L * L * ES))
+                               : make_buf(nullptr, 0u);
+
+    // ---- loads of the unit, in the order they are needed
+    {
+        const rsrc_t rk = tok_buf(a.k), rv = tok_buf(a.v);
+        u32x4 kr[NPF], vr[NPF];
 #pragma unroll
         for (int j = 0; j < NPF; ++j) {
             const int idx = tid + j * NT;
             const int t = idx / CPT, c = (idx % CPT) * VEC;
-            kpf[j] = make_uint4(0, 0, 0, 0);
-            vpf[j] = make_uint4(0, 0, 0, 0);
-            if (idx < LP * CPT && t < L) {
-                kpf[j] = *reinterpret_cast<const uint4 *>((const E *)a.k + base + (int64_t)t * a.stok + c);
-                vpf[j] = *reinterpret_cast<const uint4 *>((const E *)a.v + base + (int64_t)t * a.stok + c);
-            }
+            const uint32_t off = (idx < LP * CPT && t < L) ? (uint32_t)t * stok_b + (uint32_t)(c * ES) : kOOB;
+            kr[j] = bload16(rk, off);
+            vr[j] = bload16(rv, off);
         }
-        if (qvalid) qf.load((const E *)a.q + base + (int64_t)qi * a.stok, h2);
-        else qf.zero();
-        mpf = tid < L && (!a.mask || a.mask[r * a.L + tid] != 0);
-    };
-
-    int64_t u = unit_of(blockIdx.x, 0, nwg, a.n_units);
-    if (u < a.n_units) prefetch(u);
-    for (int64_t it = 0; u < a.n_units; ++it) {
-        const int64_t r = u / a.H;
-        const int hh = (int)(u % a.H);
-        const int64_t base = r * a.srow + (int64_t)hh * D;
-
-        // ---- move the prefetched unit into LDS
-        __syncthreads();  // the previous unit's LDS reads are done
+        const uint32_t mb = bload1(has_mask ? make_buf(a.mask + r * a.L, (uint32_t)L) : make_buf(nullptr, 0u),
+                                   (uint32_t)tid);
 #pragma unroll
         for (int j = 0; j < NPF; ++j) {
             const int idx = tid + j * NT;
             if (idx < LP * CPT) {
                 const int t = idx / CPT, c = (idx % CPT) * VEC;
-                *reinterpret_cast<uint4 *>(&k_lds[t * KSTR + c]) = kpf[j];
-                if constexpr (kTr) {
-                    *reinterpret_cast<uint4 *>(&v_lds[t * KSTR + c]) = vpf[j];
+                *reinterpret_cast<u32x4 *>(&k_lds[t * KSTR + c]) = kr[j];
+                if constexpr (kBf) {
+                    *reinterpret_cast<u32x4 *>(&v_lds[t * KSTR + c]) = vr[j];
                 } else {
-                    const E *ve = reinterpret_cast<const E *>(&vpf[j]);
+                    const E *ve = reinterpret_cast<const E *>(&vr[j]);
 #pragma unroll
                     for (int e = 0; e < VEC; ++e) v_lds[(c + e) * VSTR + t] = ve[e];
                 }
             }
         }
-        {
-            const unsigned long long bal = __ballot(mpf);  // NT >= LP: one key per thread
-            if (lane == 0) {
-                if (2 * wave < NKT) kbits[2 * wave] = (uint32_t)bal;
-                if (2 * wave + 1 < NKT) kbits[2 * wave + 1] = (uint32_t)(bal >> 32);
+        const bool keep = (!has_mask || mb != 0) && tid < L;
+        const unsigned long long bal = __ballot(keep);  // NT >= LP: one key per thread
+        if (lane == 0) {
+            if (2 * wave < NKT) kbits[2 * wave] = (uint32_t)bal;
+            if (2 * wave + 1 < NKT) kbits[2 * wave + 1] = (uint32_t)(bal >> 32);
+        }
+    }
+    ChFrag<T, D> qf;
+    qf.load(tok_buf(a.q), q_off, h2);
+    // bias of the first chunk, then the gate (needed last)
+    K32 bcur[NBB];
+    if constexpr (kBf && BV) {
+#pragma unroll
+        for (int kc = 0; kc < KC; ++kc) bcur[kc] = bias_k32<BV>(rb, qi, kc, L, h2);
+    }
+    const rsrc_t rg = has_gate ? tok_buf(a.g) : make_buf(nullptr, 0u);
+    u32x4 graw[2][NG];
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+        const int cb = 16 * half + 8 * h2;  // channels of O^T registers 8*half .. 8*half+7
+        if (16 * half >= D) continue;
+        const uint32_t off = cb < D ? q_off + (uint32_t)(cb * ES) : kOOB;
+#pragma unroll
+        for (int gi = 0; gi < NG; ++gi) graw[half][gi] = bload16(rg, off + 16u * gi);
+    }
+
+    // logits are kept as K Q^T + sqrt(d) * bias ("raw" units); the softmax
+    // scale 1/sqrt(d) and log2(e) are folded into the exponent
+    const float c2 = a.scale * kLog2e;
+    float sq_hi, sq_lo;
+    sqrt_split(D, sq_hi, sq_lo);
+    const bool two_term = sq_lo != 0.0f;
+    K32 dhi{}, dlo{};
+    if constexpr (kBf) {
+        dhi = diag_k32(sq_hi, lane);
+        if (two_term) dlo = diag_k32(sq_lo, lane);
+    }
+    const float sqd = sq_hi + sq_lo;
+    __syncthreads();
+
+    float m2 = -INFINITY;  // reference max, base-2 exponent units (per query)
+    float lsum = 0.0f;     // row sum (unused with the ones row)
+    f32x16 o = zero16();
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        // ---- the next chunk's bias goes out first (loads complete in order)
+        K32 bnext[NBB];
+        if constexpr (kBf && BV) {
+            if (c + 1 < NCH) {
+#pragma unroll
+                for (int kc = 0; kc < KC; ++kc) bnext[kc] = bias_k32<BV>(rb, qi, (c + 1) * KC + kc, L, h2);
             }
         }
-        const ChFrag<T, D> qcur = qf;
-        __syncthreads();
-
-        // ---- loads of the next unit go out now and land during the compute
-        const int64_t un = unit_of(blockIdx.x, it + 1, nwg, a.n_units);
-        if (un < a.n_units) prefetch(un);
-
-        const E *bias_row = nullptr;
-        if (a.bias && qvalid) bias_row = (const E *)a.bias + (((r / a.rpb) * a.H + hh) * (int64_t)L + qi) * L;
-
-        float m_run = -INFINITY, lsum = 0.0f;
-        f32x16 o = zero16();
-        for (int c0 = 0; c0 < NKT; c0 += KC) {
-            // ---- pass 1: logits of the chunk and their max
-            f32x16 s[KC];
-            float mx = -INFINITY;
+        // ---- pass 1: raw logits of the chunk and their max
+        f32x16 s[KC];
+        uint32_t kbs[KC];
+        float mx = -INFINITY;
 #pragma unroll
-            for (int kc = 0; kc < KC; ++kc) {
-                const int kt = c0 + kc;
-                const uint32_t kb = __builtin_amdgcn_readfirstlane(kbits[kt]);
-                if (kb == 0) continue;
-                ChFrag<T, D> kf;
-                kf.load(&k_lds[(kt * 32 + sig(n)) * KSTR], h2);
-                s[kc] = zero16();
-                ChFrag<T, D>::mma(s[kc], kf, qcur);
-                float b[16];
-                if (bias_row) {
-                    if (bias_vec && (kt + 1) * 32 <= L) {  // whole tile in range (uniform)
-                        load8_vec<T>(bias_row, kt * 32 + 8 * h2, b);
-                        load8_vec<T>(bias_row, kt * 32 + 16 + 8 * h2, b + 8);
-                    } else {
-                        load8_guarded<T>(bias_row, kt * 32 + 8 * h2, L, b);
-                        load8_guarded<T>(bias_row, kt * 32 + 16 + 8 * h2, L, b + 8);
-                    }
-                } else {
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) b[i] = 0.0f;
-                }
-                if (kb == 0xffffffffu) {
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) {
-                        s[kc][i] = __builtin_fmaf(s[kc][i], a.scale, b[i]);
-                        mx = fmaxf(mx, s[kc][i]);
-                    }
-                } else {
-                    const uint32_t kbl = kb >> (8 * h2);
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) {
-                        const float t = __builtin_fmaf(s[kc][i], a.scale, b[i]);
-                        s[kc][i] = ((kbl >> (16 * (i >> 3) + (i & 7))) & 1u) ? t : -INFINITY;
-                        mx = fmaxf(mx, s[kc][i]);
-                    }
-                }
-            }
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
-            const float m_new = fmaxf(m_run, mx);
-            // a query whose keys so far are all masked keeps o = 0 and lsum = 0
-            const float m_eff = (m_new == -INFINITY) ? 0.0f : m_new;
-            if (c0 > 0) {
-                const float alpha =
-                    (m_run == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f((m_run - m_eff) * kLog2e);
-                lsum *= alpha;
-#pragma unroll
-                for (int i = 0; i < 16; ++i) o[i] *= alpha;
-            }
-            m_run = m_new;
-            const float m2 = m_eff * kLog2e;
-            // ---- pass 2: probabilities (unnormalised), row sum, O^T += V^T P^T
-#pragma unroll
-            for (int kc = 0; kc < KC; ++kc) {
-                const int kt = c0 + kc;
-                if (__builtin_amdgcn_readfirstlane(kbits[kt]) == 0) continue;
+        for (int kc = 0; kc < KC; ++kc) {
+            const int kt = c * KC + kc;
+            // tiles whose bias is read per tile load it before any branch
+            K32 bt;
+            float bf[16];
+            if constexpr (kBf && !BV) bt = bias_k32<false>(rb, qi, kt, L, h2);
+            if constexpr (!kBf) {
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
-                    const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kc][i], kLog2e, -m2));
-                    s[kc][i] = p;
-                    lsum += p;
-                }
-                const K32 pb = Tr<T>::pack(s[kc]);
-                K32 va;
-                if constexpr (kTr) {
-                    va = load_k32_tr(v_lds, KSTR, kt * 32, D, lane);
-                } else {
-                    if (sig(n) < D) va = load_k32<T>(&v_lds[sig(n) * VSTR + kt * 32], h2);
-                    else va = zero_k32<T>();
-                }
-                Tr<T>::mma_k32(o, va, pb);
-            }
-        }
-        lsum += __shfl_xor(lsum, 32);
-
-        // ---- epilogue: normalise, gate, store O and lse
-        if (qvalid) {
-            const float inv = lsum > 0.0f ? __builtin_amdgcn_rcpf(lsum) : 0.0f;
-            const int64_t tok = base + (int64_t)qi * a.stok;
-            const E *G = a.g ? (const E *)a.g + tok : nullptr;
-            E *O = (E *)a.out + tok;
-#pragma unroll
-            for (int half = 0; half < 2; ++half) {
-                const int cb = 16 * half + 8 * h2;  // channels of regs 8*half .. 8*half+7
-                if (cb >= D) continue;
-                float val[8];
-#pragma unroll
-                for (int s8 = 0; s8 < 8; ++s8) val[s8] = o[8 * half + s8] * inv;
-                if (G) {
-                    float gv[8];
-                    load8_vec<T>(G, cb, gv);
-#pragma unroll
-                    for (int s8 = 0; s8 < 8; ++s8) val[s8] *= __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-gv[s8] * kLog2e));
-                }
-                if constexpr (sizeof(E) == 2) {
-                    uint4 w;
-                    w.x = (uint32_t)f2bf(val[0]) | ((uint32_t)f2bf(val[1]) << 16);
-                    w.y = (uint32_t)f2bf(val[2]) | ((uint32_t)f2bf(val[3]) << 16);
-                    w.z = (uint32_t)f2bf(val[4]) | ((uint32_t)f2bf(val[5]) << 16);
-                    w.w = (uint32_t)f2bf(val[6]) | ((uint32_t)f2bf(val[7]) << 16);
-                    *reinterpret_cast<uint4 *>(O + cb) = w;
-                } else {
-                    *reinterpret_cast<float4 *>(O + cb) = make_float4(val[0], val[1], val[2], val[3]);
-                    *reinterpret_cast<float4 *>(O + cb + 4) = make_float4(val[4], val[5], val[6], val[7]);
+                    const uint32_t j = (uint32_t)(kt * 32 + krow(i, h2));
+                    bf[i] = __builtin_bit_cast(float, bload4(rb, ((uint32_t)qi * L + j) * 4u));
                 }
             }
-            if (h2 == 0)
-                a.lse[(r * a.H + hh) * a.L + qi] = lsum > 0.0f ? m_run + logf(lsum) : -INFINITY;
+            const uint32_t kb = __builtin_amdgcn_readfirstlane(kbits[kt]);
+            kbs[kc] = kb;
+            if (kb == 0) continue;
+            ChFrag<T, D> kf;
+            kf.load(&k_lds[(kt * 32 + sig(n)) * KSTR], h2);
+            s[kc] = zero16();
+            ChFrag<T, D>::mma(s[kc], kf, qf);
+            if (has_bias) {
+                if constexpr (kBf) {
+                    if constexpr (BV) bt = bcur[kc];
+                    Tr<bf16_t>::mma_k32(s[kc], dhi, bt);
+                    if (two_term) Tr<bf16_t>::mma_k32(s[kc], dlo, bt);
+                } else {
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) s[kc][i] = __builtin_fmaf(bf[i], sqd, s[kc][i]);
+                }
+            }
+            if (kb != 0xffffffffu) {
+#pragma unroll
+                for (int i = 0; i < 16; ++i)
+                    s[kc][i] = __builtin_amdgcn_inverse_ballot_w64(key_lanes(kb, i)) ? s[kc][i] : -INFINITY;
+            }
+#pragma unroll
+            for (int i = 0; i < 16; i += 2) mx = fmaxf(mx, fmaxf(s[kc][i], s[kc][i + 1]));
         }
-        u = un;
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float mxl = mx * c2;
+        // raise the reference max only where a chunk max exceeds it by more
+        // than 2^kTau (always at the first finite max)
+        const bool need = mxl > m2 + kTau;
+        if (__ballot(need)) {
+            const float alpha = need ? (m2 == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2 - mxl)) : 1.0f;
+            if (need) m2 = mxl;
+            lsum *= alpha;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) o[i] *= alpha;
+        }
+        // a query whose keys so far are all masked keeps o = 0
+        const float m2e = (m2 == -INFINITY) ? 0.0f : m2;
+        // ---- pass 2: probabilities (unnormalised), row sum, O^T += V^T P^T
+#pragma unroll
+        for (int kc = 0; kc < KC; ++kc) {
+            const int kt = c * KC + kc;
+            if (kbs[kc] == 0) continue;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kc][i], c2, -m2e));
+                s[kc][i] = p;
+                if constexpr (!kOnesRow) lsum += p;
+            }
+            const K32 pb = Tr<T>::pack(s[kc]);
+            K32 va;
+            if constexpr (kBf) {
+                va = load_k32_tr(v_lds, KSTR, kt * 32, D, lane, kOnesRow);
+            } else {
+                if (sig(n) < D) va = load_k32<T>(&v_lds[sig(n) * VSTR + kt * 32], h2);
+                else va = zero_k32<T>();
+            }
+            Tr<T>::mma_k32(o, va, pb);
+        }
+        if constexpr (kBf && BV) {
+            if (c + 1 < NCH) {
+#pragma unroll
+                for (int kc = 0; kc < KC; ++kc) bcur[kc] = bnext[kc];
+            }
+        }
     }
+    if constexpr (kOnesRow) {
+        // channel D of O^T is the row sum: register 8*(D/16) + D%8 of lane half (D/8)%2
+        constexpr int ri = 8 * (D / 16) + D % 8, rh = (D / 8) % 2;
+        const float own = o[ri], other = __shfl_xor(own, 32);
+        lsum = (h2 == rh) ? own : other;
+    } else {
+        lsum += __shfl_xor(lsum, 32);
+    }
+
+    // ---- epilogue: normalise, gate, store O and lse (out-of-range lanes
+    // store to an out-of-range offset, which is dropped)
+    const float inv = lsum > 0.0f ? __builtin_amdgcn_rcpf(lsum) : 0.0f;
+    const rsrc_t ro = tok_buf(a.out);
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+        const int cb = 16 * half + 8 * h2;
+        if (16 * half >= D) continue;
+        const uint32_t off = cb < D ? q_off + (uint32_t)(cb * ES) : kOOB;
+        float gv[8];
+        if constexpr (ES == 2) {
+            const u32x4 w = graw[half][0];
+            const uint32_t ws[4] = {w.x, w.y, w.z, w.w};  // integer components (no bit_cast of a component)
+#pragma unroll
+            for (int s2 = 0; s2 < 4; ++s2) {
+                gv[2 * s2] = __builtin_bit_cast(float, ws[s2] << 16);
+                gv[2 * s2 + 1] = __builtin_bit_cast(float, ws[s2] & 0xffff0000u);
+            }
+        } else {
+#pragma unroll
+            for (int gi = 0; gi < NG; ++gi) {
+                const f32x4 w = __builtin_bit_cast(f32x4, graw[half][gi]);
+                gv[4 * gi] = w.x; gv[4 * gi + 1] = w.y; gv[4 * gi + 2] = w.z; gv[4 * gi + 3] = w.w;
+            }
+        }
+        float val[8];
+#pragma unroll
+        for (int s8 = 0; s8 < 8; ++s8) {
+            const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-gv[s8] * kLog2e));
+            val[s8] = o[8 * half + s8] * inv * (has_gate ? sg : 1.0f);
+        }
+        if constexpr (ES == 2) {
+            u32x4 w;
+            w.x = (uint32_t)f2bf(val[0]) | ((uint32_t)f2bf(val[1]) << 16);
+            w.y = (uint32_t)f2bf(val[2]) | ((uint32_t)f2bf(val[3]) << 16);
+            w.z = (uint32_t)f2bf(val[4]) | ((uint32_t)f2bf(val[5]) << 16);
+            w.w = (uint32_t)f2bf(val[6]) | ((uint32_t)f2bf(val[7]) << 16);
+            bstore16(w, ro, off);
+        } else {
+            const f32x4 w0 = {val[0], val[1], val[2], val[3]}, w1 = {val[4], val[5], val[6], val[7]};
+            bstore16(__builtin_bit_cast(u32x4, w0), ro, off);
+            bstore16(__builtin_bit_cast(u32x4, w1), ro, off + 16u);
+        }
+    }
+    // lse in natural-log units: (m2 + log2 lsum) * ln 2
+    const float lse = lsum > 0.0f ? (m2 + __builtin_amdgcn_logf(lsum)) * kLn2 : -INFINITY;
+    bstore4(__builtin_bit_cast(uint32_t, lse), make_buf(a.lse + (r * a.H + hh) * a.L, (uint32_t)L * 4u),
+            (h2 == 0 && qvalid) ? (uint32_t)qi * 4u : kOOB);
 }
 
-template <typename T, int D, int NKT>
+// key tiles per register-resident chunk: one keeps the kernel near 90
+// registers (two tiles need about 130, which halves the occupancy)
+template <int NKT> constexpr int kFwdKC = 1;
+
+template <typename T, int D, int NKT, bool BV>
 hipError_t launch_t(const Problem &p, const FwdPtrs &x, hipStream_t s) {
+    // unaligned bias rows are read per element, one tile per chunk
+    constexpr int KC = BV ? kFwdKC<NKT> : 1;
     FwdArgs a;
     a.q = x.q; a.k = x.k; a.v = x.v; a.g = x.g; a.bias = x.bias; a.mask = x.mask;
     a.out = x.out; a.lse = x.lse;
     a.L = p.L; a.rpb = p.rpb; a.srow = p.srow; a.stok = p.stok; a.H = p.H;
     a.n_units = p.N * p.H;
     a.scale = 1.0f / sqrtf((float)D);
-    // persistent grid: as many workgroups as fit on the chip at once (queried
-    // once per kernel instantiation), never more than units
-    static const int per_cu = [] {
-        int nb = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fwd_kernel<T, D, NKT>, NKT * 64, 0) != hipSuccess ||
-            nb < 1)
-            nb = 1;
-        return nb;
-    }();
-    int dev = 0, cus = 256;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
-        cus = 256;
-    int64_t nwg = (int64_t)cus * per_cu;
-    if (nwg > a.n_units) nwg = a.n_units;
-    hipLaunchKernelGGL((fwd_kernel<T, D, NKT>), dim3((unsigned)nwg), dim3(NKT * 64), 0, s, a);
+    // one workgroup per unit; the grid is rounded up to a multiple of 8 so
+    // that the XCD-aware unit order applies (surplus workgroups exit)
+    const int64_t nwg = (a.n_units + 7) / 8 * 8;
+    hipLaunchKernelGGL((fwd_kernel<T, D, NKT, KC, BV>), dim3((unsigned)nwg), dim3(NKT * 64), 0, s, a);
     return hipGetLastError();
+}
+
+template <typename T, int D, int NKT>
+hipError_t launch_t(const Problem &p, const FwdPtrs &x, hipStream_t s) {
+    // fp32 reads its bias per element either way
+    if (sizeof(typename Tr<T>::elem) == 2 && p.L % Tr<T>::VEC == 0) return launch_t<T, D, NKT, true>(p, x, s);
+    return launch_t<T, D, NKT, false>(p, x, s);
 }
 
 template <typename T, int D>

@@ -80,6 +80,24 @@ def test_ending_node_transposed_view():
     compare(got, ref, "bf16", label="ending-node")
 
 
+@pytest.mark.parametrize("dtype,d", [("bf16", 32), ("bf16", 8), ("f32", 16)])
+@pytest.mark.parametrize("sign", [1, -1])
+def test_running_max_moves(dtype, d, sign):
+    """A bias ramp of 40 along the keys makes the logits of every query grow
+    (sign 1: the running max is raised at many key tiles, each time by more
+    than the 2^8 rescale threshold) or fall (sign -1: set by the first tile)."""
+    N, L, H = 2, 256, 2
+    w, x = make_inputs(N, L, H, d, dtype, seed=21, mask="none")
+    ramp = sign * np.linspace(0.0, 40.0, L)
+    b = W.as_float64(x["bias"], dtype) + ramp[None, None, None, :]
+    x = dict(x)
+    x["bias"] = W.f32_to_bf16_bits(b.astype(np.float32)) if dtype == "bf16" else b.astype(np.float32)
+    print("\n[case] running max", dtype, d, sign, flush=True)
+    got = gpu_run(x, dtype, w.rows_per_bias)
+    ref = oracle_run(x, dtype, w.rows_per_bias)
+    compare(got, ref, dtype, label="ramp %s d%d %+d" % (dtype, d, sign))
+
+
 def test_fully_masked_rows_are_zero():
     N, L, H, d = 4, 40, 2, 16
     w, x = make_inputs(N, L, H, d, "bf16", seed=3)

@@ -26,6 +26,13 @@
 //           per chunk as a partial dBias tile.
 //   reduce  sums the partial dBias planes in chunk order.
 // Every sum has a fixed order, so all outputs are bitwise repeatable.
+//
+// Both passes keep their registers near 120 and their LDS under 80 KB so
+// that two 8-wave workgroups share a CU and hide each other's loads and
+// barriers.  Global memory is accessed through buffer instructions on
+// per-row resources with out-of-range offsets instead of branches (zeros on
+// load, dropped stores), so every load is issued unconditionally and in the
+// order it is needed.
 #include <math.h>
 #include <stdlib.h>
 
@@ -40,29 +47,36 @@ constexpr float kLog2e = 1.4426950408889634f;
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// 8 consecutive values row[j0 .. j0+7] as fp32; entries at or beyond n read as 0
-template <typename T>
-__device__ __forceinline__ void load_row8(const typename Tr<T>::elem *row, int j0, int n, bool vec_ok,
-                                          float *out8) {
+// 16 bias values of a lane as fp32: reg i <-> element j0 + 16*(i/8) + i%8 of
+// the row (the k32 order), from two 8-element groups.  BV: 16-byte aligned
+// groups (the row length is a multiple of 16 bytes / element size).
+template <typename T, bool BV>
+__device__ __forceinline__ void load_bias16(rsrc_t r, uint32_t e0, float *out16) {
     using E = typename Tr<T>::elem;
-    if (vec_ok && j0 + 8 <= n) {
-        if constexpr (sizeof(E) == 2) {
-            uint4 u = *reinterpret_cast<const uint4 *>(row + j0);
-            uint32_t w[4] = {u.x, u.y, u.z, u.w};
+    constexpr int ES = sizeof(E);
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+        const uint32_t e = e0 + 16u * g;
+        if constexpr (BV && ES == 2) {
+            const u32x4 w = bload16(r, e * 2u);
+            const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
-                out8[2 * s] = __builtin_bit_cast(float, w[s] << 16);
-                out8[2 * s + 1] = __builtin_bit_cast(float, w[s] & 0xffff0000u);
+                out16[8 * g + 2 * s] = __builtin_bit_cast(float, ws[s] << 16);
+                out16[8 * g + 2 * s + 1] = __builtin_bit_cast(float, ws[s] & 0xffff0000u);
             }
-        } else {
-            float4 a = *reinterpret_cast<const float4 *>(row + j0);
-            float4 b = *reinterpret_cast<const float4 *>(row + j0 + 4);
-            out8[0] = a.x; out8[1] = a.y; out8[2] = a.z; out8[3] = a.w;
-            out8[4] = b.x; out8[5] = b.y; out8[6] = b.z; out8[7] = b.w;
-        }
-    } else {
+        } else if constexpr (BV) {
+            const f32x4 x0 = __builtin_bit_cast(f32x4, bload16(r, e * 4u));
+            const f32x4 x1 = __builtin_bit_cast(f32x4, bload16(r, e * 4u + 16u));
+            out16[8 * g + 0] = x0.x; out16[8 * g + 1] = x0.y; out16[8 * g + 2] = x0.z; out16[8 * g + 3] = x0.w;
+            out16[8 * g + 4] = x1.x; out16[8 * g + 5] = x1.y; out16[8 * g + 6] = x1.z; out16[8 * g + 7] = x1.w;
+        } else if constexpr (ES == 2) {
 #pragma unroll
-        for (int s = 0; s < 8; ++s) out8[s] = (j0 + s < n) ? Tr<T>::to_f(row[j0 + s]) : 0.0f;
+            for (int s = 0; s < 8; ++s) out16[8 * g + s] = bf2f(bload2(r, (e + s) * 2u));
+        } else {
+#pragma unroll
+            for (int s = 0; s < 8; ++s) out16[8 * g + s] = __builtin_bit_cast(float, bload4(r, (e + s) * 4u));
+        }
     }
 }
 
@@ -98,24 +112,26 @@ struct KvArgs {
     void *dk, *dv, *dg;
     void *da;     // workspace [N][H][L][D]
     float *dsum;  // workspace [N][H][L]
-    int64_t L, rpb, srow, stok;
+    int64_t L, rpb, srow, stok, n_units;
     int H;
     float scale;
 };
 
-template <typename T, int D, int NKT>
+template <typename T, int D, int NKT, bool BV>
 __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
     using E = typename Tr<T>::elem;
     using K32 = typename Tr<T>::K32;
+    constexpr int ES = sizeof(E);
     constexpr int VEC = Tr<T>::VEC;
     constexpr int CPT = D / VEC;     // 16-byte chunks per token
     constexpr int LP = NKT * 32;
     constexpr int NT = NKT * 64;
     constexpr int RSTR = D + VEC;    // row-major LDS stride
     constexpr int TSTR = LP + VEC;   // transposed LDS stride
+    constexpr int NST = (LP * CPT + NT - 1) / NT;  // staged 16-byte chunks per thread
     // bf16: Q^T and dA^T fragments come from the transposing LDS read of the
     // row-major tiles; fp32 keeps explicit transposed copies
-    constexpr bool kTr = sizeof(E) == 2;
+    constexpr bool kTr = ES == 2;
     __shared__ __attribute__((aligned(16))) E q_lds[LP * RSTR];
     __shared__ __attribute__((aligned(16))) E da_lds[LP * RSTR];
     __shared__ __attribute__((aligned(16))) E qt_lds[kTr ? 8 : D * TSTR];
@@ -127,35 +143,66 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
     const int h2 = lane >> 5, n = lane & 31;
     const int L = (int)a.L;
     const int64_t unit = xcd_unit(blockIdx.x, gridDim.x);  // (row, head), head fastest
+    if (unit >= a.n_units) return;
     const int hh = (int)(unit % a.H);
     const int64_t r = unit / a.H;
     const int64_t b = r / a.rpb;
-    const int64_t base = r * a.srow + (int64_t)hh * D;
     const int64_t rh = r * a.H + hh;
+    const bool has_gate = a.g != nullptr, has_mask = a.mask != nullptr, has_bias = a.biasT != nullptr;
+    const uint32_t stok_b = (uint32_t)(a.stok * ES);
+    const uint32_t row_bytes = (uint32_t)(a.L * a.stok * ES);
+    const rsrc_t none = make_buf(nullptr, 0u);
+    auto tok_buf = [&](const void *X) { return make_buf((const E *)X + r * a.srow + (int64_t)hh * D, row_bytes); };
 
-    // ---- stage Q and dA (both layouts); dA, Dsum and dG come from dO, O, G here
+    // ---- every load of the unit goes out first, in the order of use:
+    // this wave's key tile (K, V as B operands, lane = key), its mask, the
+    // lse of the staged queries, the staged tokens, the first bias tile
+    const int kt = wave;
+    const int key = kt * 32 + n;
+    const bool kin = key < L;
+    const uint32_t key_off = kin ? (uint32_t)key * stok_b : kOOB;
+    ChFrag<T, D> kb, vb;
+    kb.load(tok_buf(a.k), key_off, h2);
+    vb.load(tok_buf(a.v), key_off, h2);
+    const uint32_t mbyte = bload1(has_mask ? make_buf(a.mask + r * a.L, (uint32_t)L) : none, (uint32_t)key);
+    const float lraw = __builtin_bit_cast(float, bload4(make_buf(a.lse + rh * L, (uint32_t)L * 4u),
+                                                        tid < L ? (uint32_t)tid * 4u : kOOB));
+    u32x4 qv[NST], ov[NST], dov[NST], gv[NST];
     {
-        const E *Q = (const E *)a.q + base;
-        const E *O = (const E *)a.out + base;
-        const E *dO = (const E *)a.dout + base;
-        const E *G = a.g ? (const E *)a.g + base : nullptr;
-        E *dG = a.dg ? (E *)a.dg + base : nullptr;
-        E *dAw = (E *)a.da + rh * (int64_t)L * D;
-        for (int idx = tid; idx < LP * CPT; idx += NT) {
+        const rsrc_t rq = tok_buf(a.q), ro = tok_buf(a.out), rdo = tok_buf(a.dout), rg = has_gate ? tok_buf(a.g) : none;
+#pragma unroll
+        for (int j = 0; j < NST; ++j) {
+            const int idx = tid + j * NT;
             const int t = idx / CPT, c = (idx % CPT) * VEC;
-            const bool valid = t < L;
-            uint4 qv = make_uint4(0, 0, 0, 0), ov = qv, dov = qv, gv = qv;
-            if (valid) {
-                const int64_t off = (int64_t)t * a.stok + c;
-                qv = *reinterpret_cast<const uint4 *>(Q + off);
-                ov = *reinterpret_cast<const uint4 *>(O + off);
-                dov = *reinterpret_cast<const uint4 *>(dO + off);
-                if (G) gv = *reinterpret_cast<const uint4 *>(G + off);
-            }
-            const E *oe = reinterpret_cast<const E *>(&ov);
-            const E *de = reinterpret_cast<const E *>(&dov);
-            const E *ge = reinterpret_cast<const E *>(&gv);
-            uint4 dav, dgv;
+            const uint32_t off = (idx < LP * CPT && t < L) ? (uint32_t)t * stok_b + (uint32_t)(c * ES) : kOOB;
+            qv[j] = bload16(rq, off);
+            ov[j] = bload16(ro, off);
+            dov[j] = bload16(rdo, off);
+            gv[j] = bload16(rg, off);
+        }
+    }
+    // bias^T rows of this lane's key: reg i <-> query qt*32 + krow(i, h2)
+    const rsrc_t rbt = has_bias ? make_buf((const E *)a.biasT + (b * a.H + hh) * (int64_t)L * L, (uint32_t)(L * L * ES))
+                                : none;
+    const uint32_t bt_e0 = (uint32_t)key * (uint32_t)L + 8u * h2;  // element of query 8*h2 in this key's row
+    float bcur[16];
+    load_bias16<T, BV>(rbt, bt_e0, bcur);
+
+    // ---- stage Q and dA (both layouts); dA, Dsum and dG come from dO, O, G
+    {
+        const rsrc_t rdg = has_gate ? tok_buf(a.dg) : none;
+        const rsrc_t rda = make_buf((E *)a.da + rh * (int64_t)L * D, (uint32_t)(L * D * ES));
+        const rsrc_t rds = make_buf(a.dsum + rh * L, (uint32_t)L * 4u);
+#pragma unroll
+        for (int j = 0; j < NST; ++j) {
+            const int idx = tid + j * NT;
+            const int t = idx / CPT, c = (idx % CPT) * VEC;
+            const bool in = idx < LP * CPT;
+            const bool valid = in && t < L;
+            const E *oe = reinterpret_cast<const E *>(&ov[j]);
+            const E *de = reinterpret_cast<const E *>(&dov[j]);
+            const E *ge = reinterpret_cast<const E *>(&gv[j]);
+            u32x4 dav, dgv;
             E *dae = reinterpret_cast<E *>(&dav);
             E *dge = reinterpret_cast<E *>(&dgv);
             float part = 0.0f;
@@ -163,62 +210,39 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
             for (int e = 0; e < VEC; ++e) {
                 const float o = Tr<T>::to_f(oe[e]), d = Tr<T>::to_f(de[e]);
                 part = __builtin_fmaf(d, o, part);
-                if (G) {
-                    const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-Tr<T>::to_f(ge[e]) * kLog2e));
-                    dae[e] = Tr<T>::from_f(d * sg);
-                    dge[e] = Tr<T>::from_f(d * o * (1.0f - sg));
-                } else {
-                    dae[e] = de[e];
-                }
+                const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-Tr<T>::to_f(ge[e]) * kLog2e));
+                dae[e] = has_gate ? Tr<T>::from_f(d * sg) : de[e];
+                dge[e] = Tr<T>::from_f(d * o * (1.0f - sg));
             }
             // Dsum of the token: sum over its CPT consecutive lanes
 #pragma unroll
             for (int off = 1; off < CPT; off <<= 1) part += __shfl_xor(part, off);
-            if (valid) {
-                if (dG) *reinterpret_cast<uint4 *>(dG + (int64_t)t * a.stok + c) = dgv;
-                *reinterpret_cast<uint4 *>(dAw + (int64_t)t * D + c) = dav;
-                if (c == 0) a.dsum[rh * L + t] = part;
-            }
-            if (c == 0) dsum_lds[t] = valid ? part : 0.0f;
-            *reinterpret_cast<uint4 *>(&q_lds[t * RSTR + c]) = qv;
-            *reinterpret_cast<uint4 *>(&da_lds[t * RSTR + c]) = dav;
-            if constexpr (!kTr) {
-                const E *qe = reinterpret_cast<const E *>(&qv);
+            const uint32_t toff = valid ? (uint32_t)t * stok_b + (uint32_t)(c * ES) : kOOB;
+            bstore16(dgv, rdg, toff);  // dropped without a gate
+            bstore16(dav, rda, valid ? (uint32_t)((t * D + c) * ES) : kOOB);
+            bstore4(__builtin_bit_cast(uint32_t, part), rds, (valid && c == 0) ? (uint32_t)t * 4u : kOOB);
+            if (in) {
+                if (c == 0) dsum_lds[t] = valid ? part : 0.0f;
+                *reinterpret_cast<u32x4 *>(&q_lds[t * RSTR + c]) = qv[j];
+                *reinterpret_cast<u32x4 *>(&da_lds[t * RSTR + c]) = dav;
+                if constexpr (!kTr) {
+                    const E *qe = reinterpret_cast<const E *>(&qv[j]);
 #pragma unroll
-                for (int e = 0; e < VEC; ++e) {
-                    qt_lds[(c + e) * TSTR + t] = qe[e];
-                    dat_lds[(c + e) * TSTR + t] = dae[e];
+                    for (int e = 0; e < VEC; ++e) {
+                        qt_lds[(c + e) * TSTR + t] = qe[e];
+                        dat_lds[(c + e) * TSTR + t] = dae[e];
+                    }
                 }
             }
         }
-        for (int t = tid; t < LP; t += NT) {
-            float l2 = INFINITY;  // padded or fully masked queries: P = 0
-            if (t < L) {
-                const float l = a.lse[rh * L + t];
-                if (l != -INFINITY) l2 = l * kLog2e;
-            }
-            lse2_lds[t] = l2;
-        }
+        if (tid < LP)  // padded or fully masked queries: P = 0
+            lse2_lds[tid] = (tid < L && lraw != -INFINITY) ? lraw * kLog2e : INFINITY;
     }
-
-    // ---- this wave's key tile: K and V as B operands (lane = key)
-    const int kt = wave;
-    const int key = kt * 32 + n;
-    const int arow = sig(n);  // permuted A-operand row of this lane
-    const bool kin = key < L;
-    bool kvalid = kin;
-    if (kvalid && a.mask) kvalid = a.mask[r * a.L + key] != 0;
+    const bool kvalid = kin && (!has_mask || mbyte != 0);
     const bool kfull = __ballot(kvalid) == ~0ull;
-    ChFrag<T, D> kb, vb;
-    if (kin) {
-        kb.load((const E *)a.k + base + (int64_t)key * a.stok, h2);
-        vb.load((const E *)a.v + base + (int64_t)key * a.stok, h2);
-    } else {
-        kb.zero();
-        vb.zero();
-    }
-    const E *brow = a.biasT ? (const E *)a.biasT + ((b * a.H + hh) * (int64_t)L + (kin ? key : 0)) * L : nullptr;
-    const bool bias_vec = (L % VEC) == 0;
+    const float keepf = kvalid ? 1.0f : 0.0f;  // masked key: its lane's P is 0
+    const float c2 = a.scale * kLog2e;
+    const int arow = sig(n);  // permuted A-operand row of this lane
     __syncthreads();
 
     f32x16 dv_acc = zero16(), dk_acc = zero16();
@@ -226,6 +250,9 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
 #pragma unroll
     for (int qt = 0; qt < NKT; ++qt) {
         if (qt >= nqt) break;
+        // the next tile's bias goes out first (loads complete in order)
+        float bnext[16];
+        if (qt + 1 < NKT) load_bias16<T, BV>(rbt, bt_e0 + 32u * (qt + 1), bnext);
         // S = Q K^T and dP = dA V^T for 32 queries x this wave's 32 keys;
         // lane = key, reg i = query qt*32 + krow(i, h2)
         ChFrag<T, D> qa, daa;
@@ -234,39 +261,24 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
         f32x16 S = zero16(), dP = zero16();
         ChFrag<T, D>::mma(S, qa, kb);
         ChFrag<T, D>::mma(dP, daa, vb);
-        float bv[16];
-        if (brow && bias_vec && (qt + 1) * 32 <= L && (kt + 1) * 32 <= L) {
-            // whole tile in range (uniform): two 16-byte loads of bias^T
-            load_row8<T>(brow, qt * 32 + 8 * h2, L, true, bv);
-            load_row8<T>(brow, qt * 32 + 16 + 8 * h2, L, true, bv + 8);
-        } else {
-#pragma unroll
-            for (int i = 0; i < 16; ++i) bv[i] = 0.0f;
-            if (brow && kin) {
-                load_row8<T>(brow, qt * 32 + 8 * h2, L, false, bv);
-                load_row8<T>(brow, qt * 32 + 16 + 8 * h2, L, false, bv + 8);
-            }
-        }
-        float l2[16], dsv[16];
+        f32x16 P, dS;
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
             const int q0 = qt * 32 + 16 * half + 8 * h2;
-            const float4 *lp = reinterpret_cast<const float4 *>(&lse2_lds[q0]);
-            const float4 *dp = reinterpret_cast<const float4 *>(&dsum_lds[q0]);
-            const float4 x0 = lp[0], x1 = lp[1], y0 = dp[0], y1 = dp[1];
-            l2[8 * half + 0] = x0.x; l2[8 * half + 1] = x0.y; l2[8 * half + 2] = x0.z; l2[8 * half + 3] = x0.w;
-            l2[8 * half + 4] = x1.x; l2[8 * half + 5] = x1.y; l2[8 * half + 6] = x1.z; l2[8 * half + 7] = x1.w;
-            dsv[8 * half + 0] = y0.x; dsv[8 * half + 1] = y0.y; dsv[8 * half + 2] = y0.z; dsv[8 * half + 3] = y0.w;
-            dsv[8 * half + 4] = y1.x; dsv[8 * half + 5] = y1.y; dsv[8 * half + 6] = y1.z; dsv[8 * half + 7] = y1.w;
-        }
-        f32x16 P, dS;
-        const float keepf = (kfull || kvalid) ? 1.0f : 0.0f;  // masked key: its lane's P is 0
+            const f32x4 *lp = reinterpret_cast<const f32x4 *>(&lse2_lds[q0]);
+            const f32x4 *dp = reinterpret_cast<const f32x4 *>(&dsum_lds[q0]);
+            const f32x4 l0 = lp[0], l1 = lp[1], d0 = dp[0], d1 = dp[1];
+            const float l2[8] = {l0.x, l0.y, l0.z, l0.w, l1.x, l1.y, l1.z, l1.w};
+            const float ds[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const float t = __builtin_fmaf(S[i], a.scale, bv[i]);
-            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(t, kLog2e, -l2[i])) * keepf;
-            P[i] = p;
-            dS[i] = p * (dP[i] - dsv[i]);
+            for (int s8 = 0; s8 < 8; ++s8) {
+                const int i = 8 * half + s8;
+                // log2 P = c2 * S + log2(e) * bias - lse * log2(e)
+                float p = __builtin_amdgcn_exp2f(__builtin_fmaf(S[i], c2, __builtin_fmaf(bcur[i], kLog2e, -l2[s8])));
+                if (!kfull) p *= keepf;
+                P[i] = p;
+                dS[i] = p * (dP[i] - ds[s8]);
+            }
         }
         const K32 pb = Tr<T>::pack(P);
         const K32 dsb = Tr<T>::pack(dS);
@@ -284,37 +296,43 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
         }
         Tr<T>::mma_k32(dv_acc, dat, pb);
         Tr<T>::mma_k32(dk_acc, qtf, dsb);
+        if (qt + 1 < NKT) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) bcur[i] = bnext[i];
+        }
     }
 
     // ---- dK and dV of this key tile are complete (lane = key, reg = channel)
-    if (kin) {
-        E *dKp = (E *)a.dk + base + (int64_t)key * a.stok;
-        E *dVp = (E *)a.dv + base + (int64_t)key * a.stok;
+    const rsrc_t rdk = tok_buf(a.dk), rdv = tok_buf(a.dv);
 #pragma unroll
-        for (int half = 0; half < 2; ++half) {
-            const int c0 = 16 * half + 8 * h2;
-            if (c0 >= D) continue;
-            const int o = 8 * half;
-            if constexpr (sizeof(E) == 2) {
-                uint4 wk, wv;
-                uint32_t *pk = reinterpret_cast<uint32_t *>(&wk), *pv = reinterpret_cast<uint32_t *>(&wv);
+    for (int half = 0; half < 2; ++half) {
+        const int c0 = 16 * half + 8 * h2;
+        if (16 * half >= D) continue;
+        const uint32_t off = c0 < D ? key_off + (uint32_t)(c0 * ES) : kOOB;
+        const int o = 8 * half;
+        if constexpr (ES == 2) {
+            u32x4 wk, wv;
+            uint32_t pk[4], pv[4];
 #pragma unroll
-                for (int s = 0; s < 4; ++s) {
-                    pk[s] = (uint32_t)f2bf(dk_acc[o + 2 * s] * a.scale) |
-                            ((uint32_t)f2bf(dk_acc[o + 2 * s + 1] * a.scale) << 16);
-                    pv[s] = (uint32_t)f2bf(dv_acc[o + 2 * s]) | ((uint32_t)f2bf(dv_acc[o + 2 * s + 1]) << 16);
-                }
-                *reinterpret_cast<uint4 *>(dKp + c0) = wk;
-                *reinterpret_cast<uint4 *>(dVp + c0) = wv;
-            } else {
-                *reinterpret_cast<float4 *>(dKp + c0) = make_float4(
-                    dk_acc[o] * a.scale, dk_acc[o + 1] * a.scale, dk_acc[o + 2] * a.scale, dk_acc[o + 3] * a.scale);
-                *reinterpret_cast<float4 *>(dKp + c0 + 4) = make_float4(
-                    dk_acc[o + 4] * a.scale, dk_acc[o + 5] * a.scale, dk_acc[o + 6] * a.scale, dk_acc[o + 7] * a.scale);
-                *reinterpret_cast<float4 *>(dVp + c0) = make_float4(dv_acc[o], dv_acc[o + 1], dv_acc[o + 2], dv_acc[o + 3]);
-                *reinterpret_cast<float4 *>(dVp + c0 + 4) =
-                    make_float4(dv_acc[o + 4], dv_acc[o + 5], dv_acc[o + 6], dv_acc[o + 7]);
+            for (int s2 = 0; s2 < 4; ++s2) {
+                pk[s2] = (uint32_t)f2bf(dk_acc[o + 2 * s2] * a.scale) |
+                         ((uint32_t)f2bf(dk_acc[o + 2 * s2 + 1] * a.scale) << 16);
+                pv[s2] = (uint32_t)f2bf(dv_acc[o + 2 * s2]) | ((uint32_t)f2bf(dv_acc[o + 2 * s2 + 1]) << 16);
             }
+            wk.x = pk[0]; wk.y = pk[1]; wk.z = pk[2]; wk.w = pk[3];
+            wv.x = pv[0]; wv.y = pv[1]; wv.z = pv[2]; wv.w = pv[3];
+            bstore16(wk, rdk, off);
+            bstore16(wv, rdv, off);
+        } else {
+            const f32x4 k0 = {dk_acc[o] * a.scale, dk_acc[o + 1] * a.scale, dk_acc[o + 2] * a.scale, dk_acc[o + 3] * a.scale};
+            const f32x4 k1 = {dk_acc[o + 4] * a.scale, dk_acc[o + 5] * a.scale, dk_acc[o + 6] * a.scale,
+                              dk_acc[o + 7] * a.scale};
+            const f32x4 v0 = {dv_acc[o], dv_acc[o + 1], dv_acc[o + 2], dv_acc[o + 3]};
+            const f32x4 v1 = {dv_acc[o + 4], dv_acc[o + 5], dv_acc[o + 6], dv_acc[o + 7]};
+            bstore16(__builtin_bit_cast(u32x4, k0), rdk, off);
+            bstore16(__builtin_bit_cast(u32x4, k1), rdk, off + 16u);
+            bstore16(__builtin_bit_cast(u32x4, v0), rdv, off);
+            bstore16(__builtin_bit_cast(u32x4, v1), rdv, off + 16u);
         }
     }
 }
@@ -328,22 +346,31 @@ struct QbArgs {
     const float *dsum;   // workspace [N][H][L]
     void *dq;
     float *part;         // [B][H][chunks][L][L] or null
-    int64_t L, rpb, srow, stok, chunks, rows_per_chunk;
+    int64_t L, rpb, srow, stok, chunks, rows_per_chunk, n_units;
     int H;
     float scale;
 };
 
-template <typename T, int D, int NKT>
+// dQ partials in LDS: row (wave, query) of D floats, 16-byte chunks XOR-
+// swizzled so that 16 lanes writing 16 consecutive queries hit 16 distinct
+// bank groups
+template <int D>
+__device__ __forceinline__ int dqp_index(int row, int q, int chunk) {
+    constexpr int RPB = 64 / D;  // rows per 256 bytes
+    return row * D + 4 * (chunk ^ ((q / RPB) % (D / 4)));
+}
+
+template <typename T, int D, int NKT, bool BV>
 __global__ void __launch_bounds__(NKT * 64) qbias_kernel(QbArgs a) {
     using E = typename Tr<T>::elem;
     using K32 = typename Tr<T>::K32;
-    constexpr bool kTr = sizeof(E) == 2;    // bf16: K^T fragments via the transposing LDS read
+    constexpr int ES = sizeof(E);
+    constexpr bool kTr = ES == 2;           // bf16: K^T fragments via the transposing LDS read
     constexpr int VEC = Tr<T>::VEC;
     constexpr int CPT = D / VEC;            // 16-byte chunks per token
     constexpr int LP = NKT * 32;
     constexpr int NT = NKT * 64;
     constexpr int KSTR = D + VEC;           // row stride of K, V, Q, dA tiles in LDS (elements)
-    constexpr int PSTR = D + 4;             // dQ partial stride in LDS (floats)
     constexpr int NKV = (LP * CPT + NT - 1) / NT;  // 16-byte chunks of K (and of V) per thread
     constexpr int NQC = (32 * CPT + NT - 1) / NT;  // 16-byte chunks of the Q (and dA) tile per thread
     constexpr int NSUM = (32 * (D / 4) + NT - 1) / NT;  // 4-channel groups of dQ summed per thread
@@ -354,7 +381,7 @@ __global__ void __launch_bounds__(NKT * 64) qbias_kernel(QbArgs a) {
     __shared__ __attribute__((aligned(16))) float lse2_lds[32];
     __shared__ __attribute__((aligned(16))) float dsum_lds[32];
     __shared__ uint32_t kbits_lds[NKT];
-    __shared__ __attribute__((aligned(16))) float dqp[NKT * 32 * PSTR];
+    __shared__ __attribute__((aligned(16))) float dqp[NKT * 32 * D];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int h2 = lane >> 5, n = lane & 31;
@@ -362,6 +389,7 @@ __global__ void __launch_bounds__(NKT * 64) qbias_kernel(QbArgs a) {
     const int nqt = (L + 31) / 32;
     // unit -> (b, chunk, qt, head), head fastest
     const int64_t unit = xcd_unit(blockIdx.x, gridDim.x);
+    if (unit >= a.n_units) return;
     const int hh = (int)(unit % a.H);
     int64_t rest = unit / a.H;
     const int qt = (int)(rest % nqt);
@@ -374,68 +402,69 @@ __global__ void __launch_bounds__(NKT * 64) qbias_kernel(QbArgs a) {
     const int kt = wave;
     const int qi = qt * 32 + n;  // this lane's query
     const bool qvalid = qi < L;
-    const bool vec_ok = (L % VEC) == 0;
+    const bool has_mask = a.mask != nullptr;
+    const uint32_t stok_b = (uint32_t)(a.stok * ES);
+    const uint32_t row_bytes = (uint32_t)(a.L * a.stok * ES);
+    const rsrc_t none = make_buf(nullptr, 0u);
+    const float c2 = a.scale * kLog2e;
 
-    // bias tile of (this query tile, this key tile): constant over rows
-    float bt[16];
+    // bias tile of (this query tile, this key tile), constant over rows, in
+    // base-2 exponent units: reg i <-> key kt*32 + krow(i, h2)
+    float btl[16];
+    {
+        const rsrc_t rb = a.bias ? make_buf((const E *)a.bias + (b * a.H + hh) * (int64_t)L * L, (uint32_t)(L * L * ES))
+                                 : none;
+        load_bias16<T, BV>(rb, qvalid ? (uint32_t)(qi * L + kt * 32 + 8 * h2) : kOOB / ES, btl);
 #pragma unroll
-    for (int i = 0; i < 16; ++i) bt[i] = 0.0f;
-    if (a.bias && qvalid) {
-        const E *row = (const E *)a.bias + ((b * a.H + hh) * (int64_t)L + qi) * L;
-        load_row8<T>(row, kt * 32 + 8 * h2, L, vec_ok, bt);
-        load_row8<T>(row, kt * 32 + 16 + 8 * h2, L, vec_ok, bt + 8);
+        for (int i = 0; i < 16; ++i) btl[i] *= kLog2e;
     }
     f32x16 acc = zero16();
 
-    // ---- one row's inputs, staged through registers (loads of row r+1 are in
-    // flight while row r is computed)
-    uint4 kpf[NKV], vpf[NKV], qpf[NQC], dapf[NQC];
-    float lpf = -INFINITY, dspf = 0.0f;
-    bool mpf = false;
-    auto prefetch = [&](int64_t r) {
-        const int64_t base = r * a.srow + (int64_t)hh * D;
+    // ---- one row's inputs in registers; the loads of row r+1 are issued
+    // before the dQ sum of row r
+    u32x4 kr[NKV], vr[NKV], qr[NQC], dar[NQC];
+    float lr = 0.0f, dr = 0.0f;
+    uint32_t mr = 0;
+    auto issue = [&](int64_t r) {
         const int64_t rh = r * a.H + hh;
+        const rsrc_t rk = make_buf((const E *)a.k + r * a.srow + (int64_t)hh * D, row_bytes);
+        const rsrc_t rv = make_buf((const E *)a.v + r * a.srow + (int64_t)hh * D, row_bytes);
+        const rsrc_t rq = make_buf((const E *)a.q + r * a.srow + (int64_t)hh * D, row_bytes);
+        const rsrc_t rda = make_buf((const E *)a.da + rh * (int64_t)L * D, (uint32_t)(L * D * ES));
 #pragma unroll
         for (int j = 0; j < NKV; ++j) {
             const int idx = tid + j * NT;
             const int t = idx / CPT, c = (idx % CPT) * VEC;
-            kpf[j] = make_uint4(0, 0, 0, 0);
-            vpf[j] = make_uint4(0, 0, 0, 0);
-            if (idx < LP * CPT && t < L) {
-                kpf[j] = *reinterpret_cast<const uint4 *>((const E *)a.k + base + (int64_t)t * a.stok + c);
-                vpf[j] = *reinterpret_cast<const uint4 *>((const E *)a.v + base + (int64_t)t * a.stok + c);
-            }
+            const uint32_t off = (idx < LP * CPT && t < L) ? (uint32_t)t * stok_b + (uint32_t)(c * ES) : kOOB;
+            kr[j] = bload16(rk, off);
+            vr[j] = bload16(rv, off);
         }
 #pragma unroll
         for (int j = 0; j < NQC; ++j) {
             const int idx = tid + j * NT;
             const int t = qt * 32 + idx / CPT, c = (idx % CPT) * VEC;
-            qpf[j] = make_uint4(0, 0, 0, 0);
-            dapf[j] = make_uint4(0, 0, 0, 0);
-            if (idx < 32 * CPT && t < L) {
-                qpf[j] = *reinterpret_cast<const uint4 *>((const E *)a.q + base + (int64_t)t * a.stok + c);
-                dapf[j] = *reinterpret_cast<const uint4 *>((const E *)a.da + (rh * L + t) * D + c);
-            }
+            const bool ok = idx < 32 * CPT && t < L;
+            qr[j] = bload16(rq, ok ? (uint32_t)t * stok_b + (uint32_t)(c * ES) : kOOB);
+            dar[j] = bload16(rda, ok ? (uint32_t)((t * D + c) * ES) : kOOB);
         }
-        if (tid < 32) {
-            const int t = qt * 32 + tid;
-            lpf = t < L ? a.lse[rh * L + t] : -INFINITY;
-            dspf = t < L ? a.dsum[rh * L + t] : 0.0f;
-        }
-        mpf = tid < L && (!a.mask || a.mask[r * a.L + tid] != 0);
+        const int tq = qt * 32 + (tid & 31);
+        const uint32_t qoff = tq < L ? (uint32_t)tq * 4u : kOOB;
+        lr = __builtin_bit_cast(float, bload4(make_buf(a.lse + rh * L, (uint32_t)L * 4u), qoff));
+        dr = __builtin_bit_cast(float, bload4(make_buf(a.dsum + rh * L, (uint32_t)L * 4u), qoff));
+        mr = bload1(has_mask ? make_buf(a.mask + r * a.L, (uint32_t)L) : none, (uint32_t)tid);
     };
 
-    if (r_begin < r_end) prefetch(r_begin);
+    issue(r_begin);
     for (int64_t r = r_begin; r < r_end; ++r) {
-        const int64_t base = r * a.srow + (int64_t)hh * D;
-        // ---- registers -> LDS
+        // ---- registers -> LDS (the previous row's reads of these tiles ended
+        // before its dQ-partial barrier)
 #pragma unroll
         for (int j = 0; j < NKV; ++j) {
             const int idx = tid + j * NT;
             if (idx < LP * CPT) {
                 const int t = idx / CPT, c = (idx % CPT) * VEC;
-                *reinterpret_cast<uint4 *>(&k_lds[t * KSTR + c]) = kpf[j];
-                *reinterpret_cast<uint4 *>(&v_lds[t * KSTR + c]) = vpf[j];
+                *reinterpret_cast<u32x4 *>(&k_lds[t * KSTR + c]) = kr[j];
+                *reinterpret_cast<u32x4 *>(&v_lds[t * KSTR + c]) = vr[j];
             }
         }
 #pragma unroll
@@ -443,23 +472,24 @@ __global__ void __launch_bounds__(NKT * 64) qbias_kernel(QbArgs a) {
             const int idx = tid + j * NT;
             if (idx < 32 * CPT) {
                 const int t = idx / CPT, c = (idx % CPT) * VEC;
-                *reinterpret_cast<uint4 *>(&q_lds[t * KSTR + c]) = qpf[j];
-                *reinterpret_cast<uint4 *>(&da_lds[t * KSTR + c]) = dapf[j];
+                *reinterpret_cast<u32x4 *>(&q_lds[t * KSTR + c]) = qr[j];
+                *reinterpret_cast<u32x4 *>(&da_lds[t * KSTR + c]) = dar[j];
             }
         }
         if (tid < 32) {
-            lse2_lds[tid] = (lpf == -INFINITY) ? INFINITY : lpf * kLog2e;  // fully masked query: P = 0
-            dsum_lds[tid] = dspf;
+            const bool ok = qt * 32 + tid < L && lr != -INFINITY;
+            lse2_lds[tid] = ok ? lr * kLog2e : INFINITY;  // padded or fully masked query: P = 0
+            dsum_lds[tid] = dr;
         }
         {
-            const unsigned long long bal = __ballot(mpf);  // NT >= LP: one key per thread
+            const bool keep = (!has_mask || mr != 0) && tid < L;
+            const unsigned long long bal = __ballot(keep);  // NT >= LP: one key per thread
             if (lane == 0) {
                 if (2 * wave < NKT) kbits_lds[2 * wave] = (uint32_t)bal;
                 if (2 * wave + 1 < NKT) kbits_lds[2 * wave + 1] = (uint32_t)(bal >> 32);
             }
         }
         __syncthreads();
-        if (r + 1 < r_end) prefetch(r + 1);
 
         const uint32_t kbits = __builtin_amdgcn_readfirstlane(kbits_lds[kt]);
         f32x16 dq = zero16();
@@ -475,24 +505,15 @@ __global__ void __launch_bounds__(NKT * 64) qbias_kernel(QbArgs a) {
             ChFrag<T, D>::mma(S, ka, qb);
             ChFrag<T, D>::mma(dP, va, dab);
             f32x16 dS;
-            if (kbits == 0xffffffffu) {
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const float t = __builtin_fmaf(S[i], a.scale, bt[i]);
-                    const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(t, kLog2e, -l2));
-                    dS[i] = p * (dP[i] - ds);
-                    acc[i] += dS[i];
-                }
-            } else {
-                const uint32_t kbl = kbits >> (8 * h2);
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const float t = __builtin_fmaf(S[i], a.scale, bt[i]);
-                    float p = __builtin_amdgcn_exp2f(__builtin_fmaf(t, kLog2e, -l2));
-                    p = ((kbl >> (16 * (i >> 3) + (i & 7))) & 1u) ? p : 0.0f;
-                    dS[i] = p * (dP[i] - ds);
-                    acc[i] += dS[i];
-                }
+            for (int i = 0; i < 16; ++i) {
+                float p = __builtin_amdgcn_exp2f(__builtin_fmaf(S[i], c2, btl[i] - l2));
+                if (kbits != 0xffffffffu) p = __builtin_amdgcn_inverse_ballot_w64(
+                                                  ((kbits >> krow(i, 0)) & 1u ? 0x00000000ffffffffull : 0ull) |
+                                                  ((kbits >> krow(i, 1)) & 1u ? 0xffffffff00000000ull : 0ull))
+                                                  ? p : 0.0f;
+                dS[i] = p * (dP[i] - ds);
+                acc[i] += dS[i];
             }
             // dQ^T (channels x queries) = K^T dS^T over this wave's keys
             K32 kT;
@@ -509,52 +530,60 @@ __global__ void __launch_bounds__(NKT * 64) qbias_kernel(QbArgs a) {
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
             const int c0 = 16 * half + 8 * h2;
-            if (c0 >= D) continue;
-            float *dst = &dqp[(wave * 32 + n) * PSTR + c0];
-            *reinterpret_cast<float4 *>(dst) = make_float4(dq[8 * half], dq[8 * half + 1], dq[8 * half + 2], dq[8 * half + 3]);
-            *reinterpret_cast<float4 *>(dst + 4) =
-                make_float4(dq[8 * half + 4], dq[8 * half + 5], dq[8 * half + 6], dq[8 * half + 7]);
+            if (16 * half >= D) continue;
+            if (c0 < D) {
+                const f32x4 x0 = {dq[8 * half], dq[8 * half + 1], dq[8 * half + 2], dq[8 * half + 3]};
+                const f32x4 x1 = {dq[8 * half + 4], dq[8 * half + 5], dq[8 * half + 6], dq[8 * half + 7]};
+                *reinterpret_cast<f32x4 *>(&dqp[dqp_index<D>(wave * 32 + n, n, c0 / 4)]) = x0;
+                *reinterpret_cast<f32x4 *>(&dqp[dqp_index<D>(wave * 32 + n, n, c0 / 4 + 1)]) = x1;
+            }
         }
         __syncthreads();
+        // the next row's loads go out now (the last row reloads itself)
+        issue(r + 1 < r_end ? r + 1 : r);
+        const rsrc_t rdq = make_buf((E *)a.dq + r * a.srow + (int64_t)hh * D, row_bytes);
 #pragma unroll
         for (int j = 0; j < NSUM; ++j) {  // four consecutive channels per thread and step
             const int idx = tid + j * NT;
-            if (idx >= 32 * (D / 4)) break;
-            const int q = idx / (D / 4), c = (idx % (D / 4)) * 4;
-            float4 s = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            const int q = idx / (D / 4), cq = idx % (D / 4);
+            const bool ok = idx < 32 * (D / 4);
+            f32x4 sum = {0.0f, 0.0f, 0.0f, 0.0f};
+            if (ok) {
 #pragma unroll
-            for (int w = 0; w < NKT; ++w) {
-                const float4 x = *reinterpret_cast<const float4 *>(&dqp[(w * 32 + q) * PSTR + c]);
-                s.x += x.x; s.y += x.y; s.z += x.z; s.w += x.w;
+                for (int w = 0; w < NKT; ++w) sum += *reinterpret_cast<const f32x4 *>(&dqp[dqp_index<D>(w * 32 + q, q, cq)]);
             }
-            if (qt * 32 + q < L) {
-                E *dst = (E *)a.dq + base + (int64_t)(qt * 32 + q) * a.stok + c;
-                if constexpr (sizeof(E) == 2) {
-                    uint2 w2;
-                    w2.x = (uint32_t)f2bf(s.x * a.scale) | ((uint32_t)f2bf(s.y * a.scale) << 16);
-                    w2.y = (uint32_t)f2bf(s.z * a.scale) | ((uint32_t)f2bf(s.w * a.scale) << 16);
-                    *reinterpret_cast<uint2 *>(dst) = w2;
-                } else {
-                    *reinterpret_cast<float4 *>(dst) = make_float4(s.x * a.scale, s.y * a.scale, s.z * a.scale, s.w * a.scale);
-                }
+            const uint32_t off = (ok && qt * 32 + q < L) ? (uint32_t)(qt * 32 + q) * stok_b + (uint32_t)(4 * cq * ES)
+                                                         : kOOB;
+            if constexpr (ES == 2) {
+                u32x2 w2;
+                w2.x = (uint32_t)f2bf(sum.x * a.scale) | ((uint32_t)f2bf(sum.y * a.scale) << 16);
+                w2.y = (uint32_t)f2bf(sum.z * a.scale) | ((uint32_t)f2bf(sum.w * a.scale) << 16);
+                __builtin_amdgcn_raw_buffer_store_b64(w2, rdq, off, 0, 0);
+            } else {
+                bstore16(__builtin_bit_cast(u32x4, sum * a.scale), rdq, off);
             }
         }
     }
 
     // ---- partial dBias tile of this chunk: [qi][kt*32 + krow(i, h2)]
-    if (a.part && qvalid) {
-        float *pp = a.part + (((b * a.H + hh) * a.chunks + chunk) * (int64_t)L + qi) * L;
+    if (a.part) {
+        const rsrc_t rp = make_buf(a.part + ((b * a.H + hh) * a.chunks + chunk) * (int64_t)L * L, (uint32_t)(L * L * 4));
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
             const int j0 = kt * 32 + 16 * half + 8 * h2;
-            if (j0 + 8 <= L && (L % 4) == 0) {
-                *reinterpret_cast<float4 *>(pp + j0) = make_float4(acc[8 * half], acc[8 * half + 1], acc[8 * half + 2], acc[8 * half + 3]);
-                *reinterpret_cast<float4 *>(pp + j0 + 4) =
-                    make_float4(acc[8 * half + 4], acc[8 * half + 5], acc[8 * half + 6], acc[8 * half + 7]);
+            if ((L % 8) == 0) {  // 8-key groups wholly in or out of range
+                const uint32_t off = (qvalid && j0 < L) ? (uint32_t)(qi * L + j0) * 4u : kOOB;
+                const f32x4 x0 = {acc[8 * half], acc[8 * half + 1], acc[8 * half + 2], acc[8 * half + 3]};
+                const f32x4 x1 = {acc[8 * half + 4], acc[8 * half + 5], acc[8 * half + 6], acc[8 * half + 7]};
+                bstore16(__builtin_bit_cast(u32x4, x0), rp, off);
+                bstore16(__builtin_bit_cast(u32x4, x1), rp, off + 16u);
             } else {
 #pragma unroll
-                for (int s = 0; s < 8; ++s)
-                    if (j0 + s < L) pp[j0 + s] = acc[8 * half + s];
+                for (int s8 = 0; s8 < 8; ++s8) {
+                    const float v = acc[8 * half + s8];
+                    bstore4(__builtin_bit_cast(uint32_t, v), rp,
+                            (qvalid && j0 + s8 < L) ? (uint32_t)(qi * L + j0 + s8) * 4u : kOOB);
+                }
             }
         }
     }
@@ -575,27 +604,36 @@ __global__ void __launch_bounds__(256) dbias_reduce_kernel(const float *__restri
 }
 
 // ---------------------------------------------------------------------------
-template <typename T, int D, int NKT>
-hipError_t launch_passes(const Problem &p, const KvArgs &ka, const QbArgs &qa, const BwdPlan &plan, hipStream_t s,
-                         Tracer &tr) {
-    hipLaunchKernelGGL((kv_kernel<T, D, NKT>), dim3((unsigned)(p.N * p.H)), dim3(NKT * 64), 0, s, ka);
+inline unsigned round8(int64_t n) { return (unsigned)((n + 7) / 8 * 8); }
+
+template <typename T, int D, int NKT, bool BV>
+hipError_t launch_passes(const Problem &p, const KvArgs &ka, const QbArgs &qa, hipStream_t s, Tracer &tr) {
+    // grids are rounded up to a multiple of 8 for the XCD-aware unit order;
+    // surplus workgroups exit at once
+    hipLaunchKernelGGL((kv_kernel<T, D, NKT, BV>), dim3(round8(ka.n_units)), dim3(NKT * 64), 0, s, ka);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     tr.mark(s);
-    hipLaunchKernelGGL((qbias_kernel<T, D, NKT>), dim3((unsigned)plan.n_wg), dim3(NKT * 64), 0, s, qa);
+    hipLaunchKernelGGL((qbias_kernel<T, D, NKT, BV>), dim3(round8(qa.n_units)), dim3(NKT * 64), 0, s, qa);
     e = hipGetLastError();
     if (e == hipSuccess) tr.mark(s);
     return e;
 }
 
+template <typename T, int D, int NKT>
+hipError_t launch_passes_v(const Problem &p, const KvArgs &ka, const QbArgs &qa, hipStream_t s, Tracer &tr) {
+    // BV: bias rows split into whole 16-byte groups
+    if (p.L % Tr<T>::VEC == 0) return launch_passes<T, D, NKT, true>(p, ka, qa, s, tr);
+    return launch_passes<T, D, NKT, false>(p, ka, qa, s, tr);
+}
+
 template <typename T, int D>
-hipError_t launch_passes_d(const Problem &p, const KvArgs &ka, const QbArgs &qa, const BwdPlan &plan, hipStream_t s,
-                           Tracer &tr) {
+hipError_t launch_passes_d(const Problem &p, const KvArgs &ka, const QbArgs &qa, hipStream_t s, Tracer &tr) {
     const int64_t nkt = (p.L + 31) / 32;
-    if (nkt <= 1) return launch_passes<T, D, 1>(p, ka, qa, plan, s, tr);
-    if (nkt <= 2) return launch_passes<T, D, 2>(p, ka, qa, plan, s, tr);
-    if (nkt <= 4) return launch_passes<T, D, 4>(p, ka, qa, plan, s, tr);
-    return launch_passes<T, D, 8>(p, ka, qa, plan, s, tr);
+    if (nkt <= 1) return launch_passes_v<T, D, 1>(p, ka, qa, s, tr);
+    if (nkt <= 2) return launch_passes_v<T, D, 2>(p, ka, qa, s, tr);
+    if (nkt <= 4) return launch_passes_v<T, D, 4>(p, ka, qa, s, tr);
+    return launch_passes_v<T, D, 8>(p, ka, qa, s, tr);
 }
 
 template <typename T>
@@ -623,6 +661,7 @@ hipError_t launch_bwd_t(const Problem &p, const BwdPtrs &x, void *ws, const BwdP
     ka.dk = x.dk; ka.dv = x.dv; ka.dg = x.dg;
     ka.da = w + plan.off_da; ka.dsum = (float *)(w + plan.off_dsum);
     ka.L = p.L; ka.rpb = rpb; ka.srow = p.srow; ka.stok = p.stok; ka.H = p.H; ka.scale = scale;
+    ka.n_units = p.N * p.H;
     QbArgs qa;
     qa.q = x.q; qa.k = x.k; qa.v = x.v; qa.bias = x.bias; qa.mask = x.mask; qa.lse = x.lse;
     qa.da = ka.da; qa.dsum = ka.dsum; qa.dq = x.dq;
@@ -630,10 +669,11 @@ hipError_t launch_bwd_t(const Problem &p, const BwdPtrs &x, void *ws, const BwdP
     qa.L = p.L; qa.rpb = rpb; qa.srow = p.srow; qa.stok = p.stok;
     qa.chunks = plan.chunks; qa.rows_per_chunk = plan.rows_per_chunk;
     qa.H = p.H; qa.scale = scale;
+    qa.n_units = plan.n_wg;
     switch (p.D) {
-        case 8: e = launch_passes_d<T, 8>(p, ka, qa, plan, s, tr); break;
-        case 16: e = launch_passes_d<T, 16>(p, ka, qa, plan, s, tr); break;
-        default: e = launch_passes_d<T, 32>(p, ka, qa, plan, s, tr); break;
+        case 8: e = launch_passes_d<T, 8>(p, ka, qa, s, tr); break;
+        case 16: e = launch_passes_d<T, 16>(p, ka, qa, s, tr); break;
+        default: e = launch_passes_d<T, 32>(p, ka, qa, s, tr); break;
     }
     if (e != hipSuccess || !x.bias) return e;
     const int64_t pe = p.L * p.L;
@@ -655,9 +695,11 @@ BwdPlan plan_bwd(const Problem &p, bool has_bias) {
     const int64_t rpb = has_bias ? p.rpb : p.N;
     const int64_t nqt = (p.L + 31) / 32;
     const int64_t waves = nqt <= 1 ? 1 : nqt <= 2 ? 2 : nqt <= 4 ? 4 : 8;  // per qbias workgroup
-    // qbias workgroups: enough waves to fill the chip (2048 = 8 per CU), with
-    // as few row chunks as that allows (each chunk costs one partial dBias plane)
-    int64_t target_waves = 2048;
+    // qbias workgroups: enough waves to fill the chip twice over (4096 = two
+    // 8-wave workgroups on each of 256 CUs: the kernel's registers and LDS
+    // allow two per CU), with as few row chunks as that allows (each chunk
+    // costs one partial dBias plane)
+    int64_t target_waves = 4096;
     if (const char *env = getenv("EVO_ATTN_QBIAS_WAVES")) {
         const long v = atol(env);
         if (v > 0) target_waves = v;

@@ -25,6 +25,9 @@ FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     # MFMA results straight into arch VGPRs (no accumulator-register round trip)
     "-mllvm", "-amdgpu-mfma-vgpr-form",
+    # the kernels use infinities (masks, empty rows) but never NaN: without
+    # this, every fmaxf first canonicalises both inputs (one extra VALU op each)
+    "-fno-honor-nans",
     "-Wall", "-Wno-unused-function",
     "-I", INCLUDE, "-I", CSRC,
 ]

@@ -361,7 +361,7 @@ __device__ __forceinline__ int dqp_index(int row, int q, int chunk) {
 }
 
 template <typename T, int D, int NKT, bool BV>
-__global__ void __launch_bounds__(NKT * 64) qbias_kernel(QbArgs a) {
+__global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(4))) qbias_kernel(QbArgs a) {
     using E = typename Tr<T>::elem;
     using K32 = typename Tr<T>::K32;
     constexpr int ES = sizeof(E);
@@ -420,17 +420,15 @@ __global__ void __launch_bounds__(NKT * 64) qbias_kernel(QbArgs a) {
     }
     f32x16 acc = zero16();
 
-    // ---- one row's inputs in registers; the loads of row r+1 are issued
-    // before the dQ sum of row r
+    // ---- one row's inputs in registers
     u32x4 kr[NKV], vr[NKV], qr[NQC], dar[NQC];
     float lr = 0.0f, dr = 0.0f;
     uint32_t mr = 0;
-    auto issue = [&](int64_t r) {
-        const int64_t rh = r * a.H + hh;
+    // K and V of the next row are requested during this row's exponentials,
+    // the rest (small) before the dQ sum
+    auto issue_kv = [&](int64_t r) {
         const rsrc_t rk = make_buf((const E *)a.k + r * a.srow + (int64_t)hh * D, row_bytes);
         const rsrc_t rv = make_buf((const E *)a.v + r * a.srow + (int64_t)hh * D, row_bytes);
-        const rsrc_t rq = make_buf((const E *)a.q + r * a.srow + (int64_t)hh * D, row_bytes);
-        const rsrc_t rda = make_buf((const E *)a.da + rh * (int64_t)L * D, (uint32_t)(L * D * ES));
 #pragma unroll
         for (int j = 0; j < NKV; ++j) {
             const int idx = tid + j * NT;
@@ -439,6 +437,11 @@ __global__ void __launch_bounds__(NKT * 64) qbias_kernel(QbArgs a) {
             kr[j] = bload16(rk, off);
             vr[j] = bload16(rv, off);
         }
+    };
+    auto issue_rest = [&](int64_t r) {
+        const int64_t rh = r * a.H + hh;
+        const rsrc_t rq = make_buf((const E *)a.q + r * a.srow + (int64_t)hh * D, row_bytes);
+        const rsrc_t rda = make_buf((const E *)a.da + rh * (int64_t)L * D, (uint32_t)(L * D * ES));
 #pragma unroll
         for (int j = 0; j < NQC; ++j) {
             const int idx = tid + j * NT;
@@ -454,8 +457,10 @@ __global__ void __launch_bounds__(NKT * 64) qbias_kernel(QbArgs a) {
         mr = bload1(has_mask ? make_buf(a.mask + r * a.L, (uint32_t)L) : none, (uint32_t)tid);
     };
 
-    issue(r_begin);
+    issue_kv(r_begin);
+    issue_rest(r_begin);
     for (int64_t r = r_begin; r < r_end; ++r) {
+        const int64_t rn = r + 1 < r_end ? r + 1 : r;  // the last row reloads itself
         // ---- registers -> LDS (the previous row's reads of these tiles ended
         // before its dQ-partial barrier)
 #pragma unroll
@@ -504,6 +509,7 @@ __global__ void __launch_bounds__(NKT * 64) qbias_kernel(QbArgs a) {
             f32x16 S = zero16(), dP = zero16();
             ChFrag<T, D>::mma(S, ka, qb);
             ChFrag<T, D>::mma(dP, va, dab);
+            issue_kv(rn);  // K and V are in LDS: the next row's go out now
             f32x16 dS;
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
@@ -525,6 +531,8 @@ __global__ void __launch_bounds__(NKT * 64) qbias_kernel(QbArgs a) {
                 for (int u = 0; u < 16; ++u) kT.v[u] = c < D ? k_lds[(kt * 32 + krow(u, h2)) * KSTR + c] : 0.0f;
             }
             Tr<T>::mma_k32(dq, kT, Tr<T>::pack(dS));
+        } else {
+            issue_kv(rn);
         }
         // ---- fixed-order sum of the waves' dQ partials through LDS
 #pragma unroll
@@ -539,8 +547,7 @@ __global__ void __launch_bounds__(NKT * 64) qbias_kernel(QbArgs a) {
             }
         }
         __syncthreads();
-        // the next row's loads go out now (the last row reloads itself)
-        issue(r + 1 < r_end ? r + 1 : r);
+        issue_rest(rn);
         const rsrc_t rdq = make_buf((E *)a.dq + r * a.srow + (int64_t)hh * D, row_bytes);
 #pragma unroll
         for (int j = 0; j < NSUM; ++j) {  // four consecutive channels per thread and step
@@ -549,8 +556,20 @@ __global__ void __launch_bounds__(NKT * 64) qbias_kernel(QbArgs a) {
             const bool ok = idx < 32 * (D / 4);
             f32x4 sum = {0.0f, 0.0f, 0.0f, 0.0f};
             if (ok) {
+                // partials read four at a time and added as fixed trees
+                constexpr int G = NKT < 4 ? NKT : 4;
 #pragma unroll
-                for (int w = 0; w < NKT; ++w) sum += *reinterpret_cast<const f32x4 *>(&dqp[dqp_index<D>(w * 32 + q, q, cq)]);
+                for (int w0 = 0; w0 < NKT; w0 += G) {
+                    f32x4 x[G];
+#pragma unroll
+                    for (int w = 0; w < G; ++w)
+                        x[w] = *reinterpret_cast<const f32x4 *>(&dqp[dqp_index<D>((w0 + w) * 32 + q, q, cq)]);
+#pragma unroll
+                    for (int st = 1; st < G; st *= 2)
+#pragma unroll
+                        for (int w = 0; w + st < G; w += 2 * st) x[w] += x[w + st];
+                    sum += x[0];
+                }
             }
             const uint32_t off = (ok && qt * 32 + q < L) ? (uint32_t)(qt * 32 + q) * stok_b + (uint32_t)(4 * cq * ES)
                                                          : kOOB;

@@ -508,13 +508,19 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(4
             // S^T = K Q^T, dP^T = V dA^T: lane = query, reg i = key kt*32 + krow(i, h2)
             f32x16 S = zero16(), dP = zero16();
             ChFrag<T, D>::mma(S, ka, qb);
+            if constexpr (kTr) {
+                if (kbits != 0xffffffffu) {  // masked keys: -2^64 on their rows (row n is key sig(n))
+                    const short mv = ((kbits >> sig(n)) & 1u) ? (short)0 : kBf16MaskNeg;
+                    mma_rank1(S, mv, kBf16One, h2);
+                }
+            }
             ChFrag<T, D>::mma(dP, va, dab);
             issue_kv(rn);  // K and V are in LDS: the next row's go out now
             f32x16 dS;
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
                 float p = __builtin_amdgcn_exp2f(__builtin_fmaf(S[i], c2, btl[i] - l2));
-                if (kbits != 0xffffffffu) p = __builtin_amdgcn_inverse_ballot_w64(
+                if (!kTr && kbits != 0xffffffffu) p = __builtin_amdgcn_inverse_ballot_w64(
                                                   ((kbits >> krow(i, 0)) & 1u ? 0x00000000ffffffffull : 0ull) |
                                                   ((kbits >> krow(i, 1)) & 1u ? 0xffffffff00000000ull : 0ull))
                                                   ? p : 0.0f;

@@ -299,6 +299,20 @@ __device__ __forceinline__ void sqrt_split(int d, float &hi, float &lo) {
     lo = (float)(__bf16)(r - hi);
 }
 
+// ---------------------------------------------------------------------------
+// Rank-1 MFMA term: acc[m][n] += a(m) * b(n), where a(m) is the bf16 value
+// held by lane m (lane half 0) and b(n) the one held by lane n (lane half 0):
+// one k-slot of a 32x32x8 product, the other slots zero.  With a = a large
+// negative number on masked key rows (or columns) and b = 1, it masks whole
+// key rows of a logit tile on the matrix unit instead of per logit.
+constexpr short kBf16One = 0x3F80;     // 1.0
+constexpr short kBf16MaskNeg = (short)0xDF80;  // -2^64: exp2 of any logit plus this is 0
+__device__ __forceinline__ void mma_rank1(f32x16 &acc, short a, short b, int h) {
+    const short4v av = {h == 0 ? a : (short)0, 0, 0, 0};
+    const short4v bv = {h == 0 ? b : (short)0, 0, 0, 0};
+    acc = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(av, bv, acc, 0, 0, 0);
+}
+
 __device__ __forceinline__ f32x16 zero16() {
     f32x16 z;
 #pragma unroll

@@ -104,12 +104,18 @@ __global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
     constexpr int NT = NKT * 64;
     constexpr int KSTR = D + VEC;              // row stride of K / V in LDS (elements)
     constexpr int VSTR = LP + VEC;             // row stride of V^T in LDS (fp32 path)
+    // bf16: V rows in LDS are 32 columns wide whatever the head dim, the
+    // columns past D holding constants (a 1 in column D when the row sums come
+    // from the PV product, zeros elsewhere), so the transposing read needs no
+    // per-lane substitution
+    constexpr int VSTRB = 32 + VEC;
+    constexpr int PCH = (32 - D) / 8;          // constant 16-byte chunks per V row
     constexpr int NCH = NKT / KC;              // chunks of KC key tiles
     constexpr int NPF = (LP * CPT + NT - 1) / NT;  // 16-byte chunks of K (and of V) per thread
     constexpr int NBB = kBf && BV ? KC : 1;    // bias fragments per chunk held in registers
     constexpr int NG = ES == 2 ? 1 : 2;        // 16-byte gate loads per 8 channels
     __shared__ __attribute__((aligned(16))) E k_lds[LP * KSTR];
-    __shared__ __attribute__((aligned(16))) E v_lds[kBf ? LP * KSTR : D * VSTR];
+    __shared__ __attribute__((aligned(16))) E v_lds[kBf ? LP * VSTRB : D * VSTR];
     __shared__ uint32_t kbits[NKT];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -156,12 +162,19 @@ __global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
                 const int t = idx / CPT, c = (idx % CPT) * VEC;
                 *reinterpret_cast<u32x4 *>(&k_lds[t * KSTR + c]) = kr[j];
                 if constexpr (kBf) {
-                    *reinterpret_cast<u32x4 *>(&v_lds[t * KSTR + c]) = vr[j];
+                    *reinterpret_cast<u32x4 *>(&v_lds[t * VSTRB + c]) = vr[j];
                 } else {
                     const E *ve = reinterpret_cast<const E *>(&vr[j]);
 #pragma unroll
                     for (int e = 0; e < VEC; ++e) v_lds[(c + e) * VSTR + t] = ve[e];
                 }
+            }
+        }
+        if constexpr (kBf && PCH > 0) {
+            for (int idx = tid; idx < LP * PCH; idx += NT) {
+                const int t = idx / PCH, pc = idx % PCH;
+                const u32x4 w = {(pc == 0 && kOnesRow) ? (uint32_t)(uint16_t)kBf16One : 0u, 0u, 0u, 0u};
+                *reinterpret_cast<u32x4 *>(&v_lds[t * VSTRB + D + 8 * pc]) = w;
             }
         }
         const bool keep = (!has_mask || mb != 0) && tid < L;
@@ -253,9 +266,15 @@ __global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
                 }
             }
             if (kb != 0xffffffffu) {
+                if constexpr (kBf) {
+                    // masked keys: -2^64 on their rows (row n of the tile is key sig(n))
+                    const short mv = ((kb >> sig(n)) & 1u) ? (short)0 : kBf16MaskNeg;
+                    mma_rank1(s[kc], mv, kBf16One, h2);
+                } else {
 #pragma unroll
-                for (int i = 0; i < 16; ++i)
-                    s[kc][i] = __builtin_amdgcn_inverse_ballot_w64(key_lanes(kb, i)) ? s[kc][i] : -INFINITY;
+                    for (int i = 0; i < 16; ++i)
+                        s[kc][i] = __builtin_amdgcn_inverse_ballot_w64(key_lanes(kb, i)) ? s[kc][i] : -INFINITY;
+                }
             }
 #pragma unroll
             for (int i = 0; i < 16; i += 2) mx = fmaxf(mx, fmaxf(s[kc][i], s[kc][i + 1]));
@@ -288,7 +307,7 @@ __global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
             const K32 pb = Tr<T>::pack(s[kc]);
             K32 va;
             if constexpr (kBf) {
-                va = load_k32_tr(v_lds, KSTR, kt * 32, D, lane, kOnesRow);
+                va = load_k32_tr(v_lds, VSTRB, kt * 32, 32, lane);
             } else {
                 if (sig(n) < D) va = load_k32<T>(&v_lds[sig(n) * VSTR + kt * 32], h2);
                 else va = zero_k32<T>();

@@ -20,6 +20,7 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "evo_attn_oracle.c")
+_SRCS = [_SRC, os.path.join(_HERE, "layernorm_oracle.c")]
 _LIB = os.path.join(_HERE, "liboracle_evoattn.so")
 
 _lib = None
@@ -36,7 +37,7 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB):
         tmp = _LIB + ".tmp%d" % os.getpid()
         cmd = ["gcc", "-std=c11", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra",
-               "-o", tmp, _SRC, "-lm"]
+               "-o", tmp] + _SRCS + ["-lm"]
         subprocess.run(cmd, check=True)
         os.replace(tmp, _LIB)
     return _LIB
@@ -45,7 +46,7 @@ def build(force: bool = True) -> str:
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < max(map(os.path.getmtime, _SRCS)):
             build(force=True)
         lib = ctypes.CDLL(_LIB)
         P = ctypes.c_void_p
@@ -56,6 +57,10 @@ def _load():
         for f in (lib.evo_oracle_fwd, lib.evo_oracle_bwd, lib.evo_oracle_probs):
             f.restype = ctypes.c_int
         lib.evo_oracle_threads.restype = ctypes.c_int
+        I, D = ctypes.c_int64, ctypes.c_double
+        lib.ln_oracle_fwd.argtypes = [I, I, D] + [P] * 6
+        lib.ln_oracle_bwd.argtypes = [I, I, D] + [P] * 6
+        lib.ln_oracle_fwd.restype = lib.ln_oracle_bwd.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -131,3 +136,40 @@ def probs(q, k, bias=None, mask=None, row: int = 0, head: int = 0,
     if st:
         raise ValueError("oracle probs failed with status %d" % st)
     return P
+
+
+def layernorm_forward(x, weight=None, bias=None, eps: float = 1e-5):
+    """LayerNorm over the last axis: (y, mean, rstd), y shaped like x, the
+    statistics shaped like x without its last axis (layernorm_oracle.c)."""
+    x = _f64(x)
+    C = x.shape[-1]
+    R = x.size // C if C else 0
+    w, b = _f64(weight), _f64(bias)
+    for p_ in (w, b):
+        if p_ is not None and p_.shape != (C,):
+            raise ValueError("weight and bias must have shape (%d,)" % C)
+    y = np.zeros_like(x)
+    mean = np.zeros(x.shape[:-1], np.float64)
+    rstd = np.zeros(x.shape[:-1], np.float64)
+    st = _load().ln_oracle_fwd(R, C, float(eps), _ptr(x), _ptr(w), _ptr(b), _ptr(y),
+                               _ptr(mean), _ptr(rstd))
+    if st:
+        raise ValueError("oracle layernorm forward failed with status %d" % st)
+    return y, mean, rstd
+
+
+def layernorm_backward(x, dy, weight=None, eps: float = 1e-5):
+    """Gradients (dx, dweight, dbias) of the LayerNorm above for upstream dy."""
+    x, dy, w = _f64(x), _f64(dy), _f64(weight)
+    if dy.shape != x.shape:
+        raise ValueError("dy must be shaped like x")
+    C = x.shape[-1]
+    R = x.size // C if C else 0
+    dx = np.zeros_like(x)
+    dw = np.zeros(C, np.float64)
+    db = np.zeros(C, np.float64)
+    st = _load().ln_oracle_bwd(R, C, float(eps), _ptr(x), _ptr(w), _ptr(dy), _ptr(dx),
+                               _ptr(dw), _ptr(db))
+    if st:
+        raise ValueError("oracle layernorm backward failed with status %d" % st)
+    return dx, dw, db

@@ -83,10 +83,11 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-baseline duration")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (reference for HBM byte counters)")
-    ap.add_argument("--source-hash", action="store_true", help="print the kernel-source hash and exit")
+    ap.add_argument("--source-hash", nargs="?", const="attn", default=None, choices=sorted(KERNEL_SOURCES),
+                    help="print the source hash of a kernel family (attn, ln) and exit")
     args = ap.parse_args()
     if args.source_hash:
-        print(kernel_source_hash())
+        print(kernel_source_hash(args.source_hash))
         return
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -100,6 +101,10 @@ def main():
 
     if args.copy_calibration:
         copy_calibration(torch, args.copy_calibration, max(args.steps, 1))
+        return
+
+    if args.workload.startswith("ln_"):
+        ln_bench(torch, args)
         return
 
     w = W.by_name(args.workload)
@@ -170,9 +175,33 @@ def main():
         e1.record(stream)
         bwd(evs)
     torch.cuda.synchronize()
-    fwd_ms = float(np.mean([a.elapsed_time(b) for a, b in fev]))
-    bwd_ms = float(np.mean([l_[0].elapsed_time(l_[-1]) for l_ in bev]))
+    fwd_warm = [a.elapsed_time(b) for a, b in fev]
+    bwd_warm = [l_[0].elapsed_time(l_[-1]) for l_ in bev]
+    fwd_ms = float(np.mean(fwd_warm))
+    bwd_ms = float(np.mean(bwd_warm))
     kern_ms = [fwd_ms] + [float(np.mean([l_[j].elapsed_time(l_[j + 1]) for l_ in bev])) for j in range(nk)]
+
+    # cold mode: a 512 MiB scratch buffer is written before every timed call
+    # (outside the events), which evicts the inputs from L2 and the Infinity
+    # Cache, so each call reads them from HBM
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    cev = [[mk() for _ in range(4)] for _ in range(args.steps)]
+    for e in [x for l_ in cev for x in l_]:
+        e.record(stream)
+    torch.cuda.synchronize()
+    for e0, e1, e2, e3 in cev:
+        flush.fill_(1)
+        e0.record(stream)
+        fwd()
+        e1.record(stream)
+        flush.fill_(2)
+        e2.record(stream)
+        bwd()
+        e3.record(stream)
+    torch.cuda.synchronize()
+    fwd_cold = [l_[0].elapsed_time(l_[1]) for l_ in cev]
+    bwd_cold = [l_[2].elapsed_time(l_[3]) for l_ in cev]
+    del flush
 
     flops = w.flops_fwd() + w.flops_bwd()
     tflops = flops / (ms_step * 1e-3) / 1e12
@@ -213,7 +242,18 @@ def main():
         "config": {"workload": w.name, "n_rows": N, "seq_len": L, "n_heads": H, "head_dim": d,
                    "rows_per_bias": rpb, "bias": w.bias, "gate": w.gate, "mask": w.mask,
                    "parallelism": "single-gpu"},
-        "fwd_ms": round(fwd_ms, 5), "bwd_ms": round(bwd_ms, 5), "kernels": kernels,
+        "fwd_ms": round(fwd_ms, 5), "bwd_ms": round(bwd_ms, 5),
+        "fwd_tflops": round(w.flops_fwd() / (fwd_ms * 1e-3) / 1e12, 2),
+        "bwd_tflops": round(w.flops_bwd() / (bwd_ms * 1e-3) / 1e12, 2),
+        "timing": {
+            "warm": {"note": "calls back to back, inputs resident in HBM and partly in caches",
+                     "fwd_ms": _pct(fwd_warm), "bwd_ms": _pct(bwd_warm)},
+            "cold": {"note": "512 MiB scratch written before each call, outside the events",
+                     "fwd_ms": _pct(fwd_cold), "bwd_ms": _pct(bwd_cold),
+                     "fwd_bwd_tflops_median": round(flops / ((np.median(fwd_cold) + np.median(bwd_cold))
+                                                             * 1e-3) / 1e12, 2)},
+        },
+        "kernels": kernels,
         "fwd_bwd_frac_of_mfma_peak": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
         "fwd_bwd_hbm_gbs": round((fwd_bytes + bwd_bytes) / (ms_step * 1e-3) / 1e9, 1),
         "wall_s": round(wall, 3),
@@ -221,6 +261,170 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(line))
+
+
+def ln_bench(torch, args):
+    """LayerNorm forward + backward on one of the LayerNorm workloads: one step
+    is evo_layernorm_fwd + evo_layernorm_bwd over the whole [R, C] tensor.
+    `value` is algorithmic HBM bytes of the step (each tensor touched once)
+    per second; the roofline is the HBM bound of the dominant kernel."""
+    from paper_2404_11068_amd import layernorm as ln
+    from paper_2404_11068_amd import workloads as W
+
+    w = W.ln_by_name(args.workload)
+    x = W.generate_ln(w)
+    es = 2 if w.dtype == "bf16" else 4
+
+    def dev(a):
+        if w.dtype == "bf16":
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+
+    xd, dyd = dev(x["x"]), dev(x["dy"])
+    wt, bt = torch.from_numpy(x["weight"]).cuda(), torch.from_numpy(x["bias"]).cuda()
+    R, C = w.n_rows, w.n_cols
+    y = torch.empty_like(xd)
+    dx = torch.empty_like(xd)
+    mean = torch.empty(R, dtype=torch.float32, device="cuda")
+    rstd = torch.empty(R, dtype=torch.float32, device="cuda")
+    dw = torch.empty(C, dtype=torch.float32, device="cuda")
+    db = torch.empty(C, dtype=torch.float32, device="cuda")
+    ws_bytes = ln.workspace_size(xd, w.eps)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    n_part = ws_bytes // (2 * C * 4)
+    stream = torch.cuda.current_stream()
+
+    def fwd():
+        ln.layernorm_fwd(xd, wt, bt, w.eps, y=y, mean=mean, rstd=rstd, stream=stream)
+
+    def bwd(events=None):
+        ln.layernorm_bwd(xd, wt, mean, rstd, dyd, dx=dx, dweight=dw, dbias=db, workspace=ws, eps=w.eps,
+                         stream=stream, events=events)
+
+    for _ in range(args.warmup):
+        fwd()
+        bwd()
+    torch.cuda.synchronize()
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    start, stop = mk(), mk()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record(stream)
+    for _ in range(args.steps):
+        fwd()
+        bwd()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = start.elapsed_time(stop) / args.steps
+
+    fev = [(mk(), mk()) for _ in range(args.steps)]
+    bev = [[mk() for _ in range(3)] for _ in range(args.steps)]
+    for e in [e for p_ in fev for e in p_] + [e for l_ in bev for e in l_]:
+        e.record(stream)
+    torch.cuda.synchronize()
+    for (e0, e1), evs in zip(fev, bev):
+        e0.record(stream)
+        fwd()
+        e1.record(stream)
+        bwd(evs)
+    torch.cuda.synchronize()
+    fwd_warm = [a.elapsed_time(b) for a, b in fev]
+    bwd_warm = [l_[0].elapsed_time(l_[2]) for l_ in bev]
+    k_ms = [float(np.mean(fwd_warm)), float(np.mean([l_[0].elapsed_time(l_[1]) for l_ in bev])),
+            float(np.mean([l_[1].elapsed_time(l_[2]) for l_ in bev]))]
+
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    cev = [[mk() for _ in range(4)] for _ in range(args.steps)]
+    for e in [e for l_ in cev for e in l_]:
+        e.record(stream)
+    torch.cuda.synchronize()
+    for e0, e1, e2, e3 in cev:
+        flush.fill_(1)
+        e0.record(stream)
+        fwd()
+        e1.record(stream)
+        flush.fill_(2)
+        e2.record(stream)
+        bwd()
+        e3.record(stream)
+    torch.cuda.synchronize()
+    fwd_cold = [l_[0].elapsed_time(l_[1]) for l_ in cev]
+    bwd_cold = [l_[2].elapsed_time(l_[3]) for l_ in cev]
+    del flush
+
+    tok = R * C * es
+    part = n_part * 2 * C * 4
+    model = [("ln_fwd_kernel", 2 * tok + 8 * R + 8 * C),
+             ("ln_bwd_kernel", 3 * tok + 8 * R + 4 * C + part),
+             ("ln_param_reduce", part + 8 * C)]
+    kernels = {}
+    for (name, nbytes), ms in zip(model, k_ms):
+        kernels[name] = {"avg_ms": round(ms, 5), "algorithmic_bytes": int(nbytes),
+                         "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1)}
+    dom = max(range(len(model)), key=lambda i: k_ms[i])
+    dname, dbytes = model[dom]
+    ach = dbytes / (k_ms[dom] * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": measured_traffic(dname, w.name),
+                "kernel": dname, "avg_ms": round(k_ms[dom], 5), "algorithmic_bytes": int(dbytes)}
+    step_bytes = w.bytes_fwd() + w.bytes_bwd()
+    cpu = None if args.no_cpu_baseline else ln_cpu_baseline(w, x, args.cpu_seconds)
+    line = {
+        "metric": "LayerNorm fwd+bwd throughput (algorithmic HBM bytes per second) on 1 MI355X",
+        "value": round(step_bytes / (ms_step * 1e-3) / 1e9, 1), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "n_rows": R, "n_cols": C, "eps": w.eps, "parallelism": "single-gpu"},
+        "fwd_ms": round(k_ms[0], 5), "bwd_ms": round(float(np.mean(bwd_warm)), 5),
+        "fwd_gbs": round(w.bytes_fwd() / (k_ms[0] * 1e-3) / 1e9, 1),
+        "bwd_gbs": round(w.bytes_bwd() / (float(np.mean(bwd_warm)) * 1e-3) / 1e9, 1),
+        "timing": {
+            "warm": {"note": "calls back to back, inputs resident in HBM and partly in caches",
+                     "fwd_ms": _pct(fwd_warm), "bwd_ms": _pct(bwd_warm)},
+            "cold": {"note": "512 MiB scratch written before each call, outside the events",
+                     "fwd_ms": _pct(fwd_cold), "bwd_ms": _pct(bwd_cold),
+                     "fwd_bwd_gbs_median": round(step_bytes / ((np.median(fwd_cold) + np.median(bwd_cold))
+                                                               * 1e-3) / 1e9, 1)},
+        },
+        "kernels": kernels, "wall_s": round(wall, 3), "roofline": roofline, "cpu_baseline": cpu,
+    }
+    print(json.dumps(line))
+
+
+def ln_cpu_baseline(w, x, target_s: float):
+    """The fp64 LayerNorm oracle (forward + backward) on the host cores, on
+    the whole workload repeated (or a slice of rows) for about target_s."""
+    import oracle
+    from paper_2404_11068_amd import workloads as W
+
+    xf = W.as_float64(x["x"], w.dtype)
+    dyf = W.as_float64(x["dy"], w.dtype)
+    wf, bf = x["weight"].astype(np.float64), x["bias"].astype(np.float64)
+
+    def run(rows):
+        t0 = time.perf_counter()
+        oracle.layernorm_forward(xf[:rows], wf, bf, w.eps)
+        oracle.layernorm_backward(xf[:rows], dyf[:rows], wf, w.eps)
+        return time.perf_counter() - t0
+
+    rows = w.n_rows
+    t = run(rows)
+    reps = max(1, int(target_s / max(t, 1e-3)))
+    t = float(np.median([run(rows) for _ in range(reps)]))
+    return {"value": round((w.bytes_fwd() + w.bytes_bwd()) / t / 1e9, 3), "unit": "GB/s",
+            "cores": oracle.threads(), "kind": "oracle", "cpu_model": _cpu_model(),
+            "seconds_per_run": round(t, 4), "runs": reps,
+            "sample": "whole workload (%d x %d), forward + backward in fp64 (OpenMP rows), median of %d runs"
+                      % (w.n_rows, w.n_cols, reps)}
+
+
+def _pct(xs):
+    """median and 10th/90th percentiles of per-call times in ms"""
+    a = np.asarray(xs, dtype=np.float64)
+    return {"median": round(float(np.median(a)), 5), "p10": round(float(np.percentile(a, 10)), 5),
+            "p90": round(float(np.percentile(a, 90)), 5), "n": int(a.size)}
 
 
 def measured_traffic(kernel: str, workload: str):
@@ -236,21 +440,30 @@ def measured_traffic(kernel: str, workload: str):
         return None
     for e in entries.get("entries", []):
         if e.get("kernel") == kernel and e.get("workload") == workload:
-            if e.get("source_sha256") != kernel_source_hash():
+            if e.get("source_sha256") != kernel_source_hash(kernel_family(kernel)):
                 return None
             return e.get("bytes_per_launch")
     return None
 
 
-def kernel_source_hash() -> str:
-    """sha256 over the HIP sources and headers that define the kernels."""
+# device sources of each kernel family (a change to any of them invalidates
+# the family's recorded counters)
+KERNEL_SOURCES = {"attn": ("evo_frag.h", "evo_fwd.hip", "evo_bwd.hip"),
+                  "ln": ("evo_frag.h", "evo_ln.hip")}
+
+
+def kernel_family(kernel: str) -> str:
+    return "ln" if kernel.startswith("ln_") else "attn"
+
+
+def kernel_source_hash(family: str = "attn") -> str:
+    """sha256 over the HIP sources that define one family's kernels."""
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2404_11068_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
-        if name.endswith((".hip", ".h", ".cpp")):
-            with open(os.path.join(csrc, name), "rb") as f:
-                h.update(name.encode() + b"\0" + f.read())
+    for name in KERNEL_SOURCES[family]:
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()
 
 
@@ -289,11 +502,16 @@ def cpu_baseline(w, x, target_s: float):
         g = None if x["gate"] is None else f(x["gate"][sl])
         b = None if x["bias"] is None else f(x["bias"])[: max(rows // rpb, 1)]
         m = None if x["mask"] is None else x["mask"][sl]
-        t = time.perf_counter()
+        do = f(x["dout"][sl])
+        t0 = time.perf_counter()
         oracle.forward(*args, g, b, m, rpb)
-        oracle.backward(*args, f(x["dout"][sl]), g, b, m, rpb)
-        return time.perf_counter() - t
+        t1 = time.perf_counter()
+        oracle.backward(*args, do, g, b, m, rpb)
+        t2 = time.perf_counter()
+        split.append((t1 - t0, t2 - t1))
+        return t2 - t0
 
+    split = []
     rows = max(1, min(w.n_rows, 4))
     t = run(rows)
     # grow the sample to roughly target_s of CPU work (bounded by the workload)
@@ -302,16 +520,31 @@ def cpu_baseline(w, x, target_s: float):
     # a sample of at least one whole bias plane keeps whole planes
     if w.bias and want >= w.rows_per_bias:
         want = (want // w.rows_per_bias) * w.rows_per_bias
+    split.clear()
     t = run(want)
     reps = 1
     if want == w.n_rows and t < target_s:  # the whole workload is short: repeat it
         reps = max(1, int(target_s / max(t, 1e-3)))
         t = sum(run(want) for _ in range(reps)) / reps
     flops = (w.flops_fwd() + w.flops_bwd()) * want / w.n_rows
+    tf = float(np.median([a for a, _ in split]))
+    tb = float(np.median([b_ for _, b_ in split]))
     return {"value": round(flops / t / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.threads(),
-            "kind": "oracle", "seconds_per_run": round(t, 3), "runs": reps,
+            "kind": "oracle", "cpu_model": _cpu_model(), "seconds_per_run": round(t, 3), "runs": reps,
+            "fwd_s_median": round(tf, 3), "bwd_s_median": round(tb, 3),
             "sample": "%d of %d rows of %s, forward + backward in fp64 (OpenMP), mean of %d run(s)"
                       % (want, w.n_rows, w.name, reps)}
+
+
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 if __name__ == "__main__":

@@ -16,7 +16,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libevoattn.so")
 OBJDIR = os.path.join(PKG, "_build")
 
-SOURCES = ["evo_fwd.hip", "evo_bwd.hip", "evo_api.cpp"]
+SOURCES = ["evo_fwd.hip", "evo_bwd.hip", "evo_ln.hip", "evo_api.cpp", "evo_ln_api.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

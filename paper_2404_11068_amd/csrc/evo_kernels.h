@@ -60,4 +60,32 @@ hipError_t launch_fwd(const Problem &p, const FwdPtrs &x, hipStream_t s);
 hipError_t launch_bwd(const Problem &p, const BwdPtrs &x, void *ws, const BwdPlan &plan,
                       hipStream_t s, Tracer *tr = nullptr);
 
+// LayerNorm over the last axis of a contiguous [R, C] tensor
+struct LnProblem {
+    int dtype;   // 0 = fp32, 1 = bf16 (x, y, dy, dx); parameters and statistics are fp32
+    int C;
+    int64_t R;
+    float eps;
+};
+
+struct LnPtrs {
+    const void *x;
+    const float *w, *b;
+    void *y;
+    float *mean, *rstd;  // nullable
+};
+
+struct LnBwdPtrs {
+    const void *x;
+    const float *w, *mean, *rstd;
+    const void *dy;
+    void *dx;
+    float *dw, *db;
+};
+
+bool ln_supported_cols(int C);
+size_t ln_bwd_workspace(const LnProblem &p);
+hipError_t launch_ln_fwd(const LnProblem &p, const LnPtrs &x, hipStream_t s);
+hipError_t launch_ln_bwd(const LnProblem &p, const LnBwdPtrs &x, void *ws, hipStream_t s, Tracer *tr = nullptr);
+
 }  // namespace evo

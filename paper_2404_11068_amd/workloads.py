@@ -165,3 +165,67 @@ def generate(w: Workload, seed: Optional[int] = None, with_dout: bool = True) ->
     out["mask"] = _mask(w, rng, N, L)
     out["dout"] = _store(rng.standard_normal(shape), w.dtype) if with_dout else None
     return out
+
+
+# ---------------------------------------------------------------------------
+# LayerNorm workloads: the normalisations in front of the Evoformer blocks at
+# the 256-residue crop (ScaleFold Section 3.3, "LayerNormalization": rows of
+# 128 and 256 channels, plus the 64-channel extra-MSA stack).  x rows get a
+# per-row offset and spread, as residual-stream activations do; the weight and
+# bias sit near the identity transform, as trained LayerNorm parameters do.
+# Draw order: row offset, row spread, x, weight, bias, dy.
+
+@dataclasses.dataclass(frozen=True)
+class LnWorkload:
+    name: str
+    n_rows: int
+    n_cols: int
+    dtype: str
+    eps: float = 1e-5
+    seed: int = 0
+    description: str = ""
+
+    def bytes_fwd(self) -> int:
+        es = 2 if self.dtype == "bf16" else 4
+        # x in, y out, mean and rstd out, weight and bias in
+        return 2 * self.n_rows * self.n_cols * es + 8 * self.n_rows + 8 * self.n_cols
+
+    def bytes_bwd(self) -> int:
+        es = 2 if self.dtype == "bf16" else 4
+        # x and dy in, dx out, mean and rstd in, weight in, dweight and dbias out
+        return 3 * self.n_rows * self.n_cols * es + 8 * self.n_rows + 12 * self.n_cols
+
+
+LN_WORKLOADS = [
+    LnWorkload("ln_tiny_f32", 77, 64, "f32", seed=2000,
+               description="tiny fp32 check: 77 rows x 64 channels"),
+    LnWorkload("ln_msa_bf16", 128 * 256, 256, "bf16", seed=2001,
+               description="MSA representation: 128 sequences x 256 residues, c_m = 256"),
+    LnWorkload("ln_pair_bf16", 256 * 256, 128, "bf16", seed=2002,
+               description="pair representation: 256 x 256 residue pairs, c_z = 128"),
+    LnWorkload("ln_extra_msa_bf16", 1024 * 256, 64, "bf16", seed=2003,
+               description="extra-MSA representation: 1024 sequences x 256 residues, c_e = 64"),
+]
+
+
+def ln_by_name(name: str) -> LnWorkload:
+    for w in LN_WORKLOADS:
+        if w.name == name:
+            return w
+    raise KeyError(name)
+
+
+def generate_ln(w: LnWorkload, seed: Optional[int] = None, n_rows: Optional[int] = None
+                ) -> Dict[str, np.ndarray]:
+    """x, dy: [R, C]; weight, bias: [C] fp32.  x and dy are stored as fp32 or
+    bf16 bits (w.dtype); the parameters are always fp32."""
+    rng = np.random.Generator(np.random.PCG64(w.seed if seed is None else seed))
+    R = w.n_rows if n_rows is None else n_rows
+    C = w.n_cols
+    offset = rng.standard_normal((R, 1)) * 2.0
+    spread = rng.uniform(0.25, 4.0, size=(R, 1))
+    x = rng.standard_normal((R, C)) * spread + offset
+    weight = (1.0 + 0.2 * rng.standard_normal(C)).astype(np.float32)
+    bias = (0.2 * rng.standard_normal(C)).astype(np.float32)
+    dy = rng.standard_normal((R, C))
+    return {"x": _store(x, w.dtype), "weight": weight, "bias": bias, "dy": _store(dy, w.dtype)}

@@ -173,3 +173,30 @@ def layernorm_backward(x, dy, weight=None, eps: float = 1e-5):
     if st:
         raise ValueError("oracle layernorm backward failed with status %d" % st)
     return dx, dw, db
+
+
+def ln_proj_forward(x, ln_weight, ln_bias, weight, bias=None, n_proj: int = 1, eps: float = 1e-5):
+    """LayerNorm over the last axis followed by n_proj independent linear
+    projections that share the normalised input (ScaleFold Section 3.3,
+    "GEMM Batching": the four linear layers in front of the attention have
+    no dependency on each other and run as one batched product).
+
+    x [..., C]; weight [n_proj * HD, C] (torch Linear layout: row f of
+    projection p is weight[p * HD + f]); bias [n_proj * HD] or None.
+    Returns a list of n_proj arrays [..., HD]:
+        out_p = LN(x) @ weight[p*HD:(p+1)*HD].T + bias[p*HD:(p+1)*HD]
+    The matmul is a library primitive (numpy, fp64)."""
+    x = _f64(x)
+    W = _f64(weight)
+    C = x.shape[-1]
+    if W.ndim != 2 or W.shape[1] != C or W.shape[0] % n_proj:
+        raise ValueError("weight must be [n_proj * HD, C]")
+    HD = W.shape[0] // n_proj
+    y, _, _ = layernorm_forward(x, ln_weight, ln_bias, eps)
+    outs = []
+    for p in range(n_proj):
+        o = y @ W[p * HD:(p + 1) * HD].T
+        if bias is not None:
+            o = o + _f64(bias)[p * HD:(p + 1) * HD]
+        outs.append(o)
+    return outs

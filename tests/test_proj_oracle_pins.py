@@ -1,0 +1,79 @@
+"""Pins for the oracle of the fused LayerNorm + batched projections.
+
+* a library routine: torch-CPU fp64 layer_norm followed by torch linear,
+  one call per projection;
+* special cases: an identity weight returns the normalised input itself,
+  rows of a permutation matrix pick its channels, a zero weight returns the
+  bias;
+* structure: n_proj projections equal one projection with the stacked
+  weight, split; rows are independent; the output is linear in the weight.
+"""
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import oracle
+
+
+def _case(seed, R=9, C=16, HD=8, P=4, bias=True):
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((R, C)) * 2.0 + 0.5
+    lw = 1.0 + 0.3 * rng.standard_normal(C)
+    lb = 0.3 * rng.standard_normal(C)
+    W = rng.standard_normal((P * HD, C)) / np.sqrt(C)
+    b = rng.standard_normal(P * HD) if bias else None
+    return x, lw, lb, W, b
+
+
+@pytest.mark.parametrize("P,bias", [(1, False), (2, True), (4, True), (4, False)])
+def test_matches_torch(P, bias):
+    x, lw, lb, W, b = _case(1, P=P, bias=bias)
+    outs = oracle.ln_proj_forward(x, lw, lb, W, b, n_proj=P, eps=1e-5)
+    y = F.layer_norm(torch.tensor(x), (x.shape[-1],), torch.tensor(lw), torch.tensor(lb), 1e-5)
+    HD = W.shape[0] // P
+    for p in range(P):
+        ref = F.linear(y, torch.tensor(W[p * HD:(p + 1) * HD]),
+                       None if b is None else torch.tensor(b[p * HD:(p + 1) * HD]))
+        np.testing.assert_allclose(outs[p], ref.numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_identity_permutation_and_zero_weights():
+    x, lw, lb, _, _ = _case(2, C=8)
+    y, _, _ = oracle.layernorm_forward(x, lw, lb, 1e-5)
+    (o,) = oracle.ln_proj_forward(x, lw, lb, np.eye(8), None, n_proj=1)
+    np.testing.assert_allclose(o, y, rtol=0, atol=1e-15)
+    perm = np.array([3, 0, 7, 5, 1, 2, 6, 4])
+    a, b_ = oracle.ln_proj_forward(x, lw, lb, np.eye(8)[np.concatenate([perm, perm[::-1]])], None, n_proj=2)
+    np.testing.assert_allclose(a, y[:, perm], rtol=0, atol=1e-15)
+    np.testing.assert_allclose(b_, y[:, perm[::-1]], rtol=0, atol=1e-15)
+    bias = np.arange(16.0)
+    outs = oracle.ln_proj_forward(x, lw, lb, np.zeros((16, 8)), bias, n_proj=4)
+    for p in range(4):
+        np.testing.assert_array_equal(outs[p], np.broadcast_to(bias[4 * p:4 * p + 4], (x.shape[0], 4)))
+
+
+def test_split_rows_and_linearity():
+    x, lw, lb, W, b = _case(3)
+    outs = oracle.ln_proj_forward(x, lw, lb, W, b, n_proj=4)
+    (whole,) = oracle.ln_proj_forward(x, lw, lb, W, b, n_proj=1)
+    np.testing.assert_allclose(np.concatenate(outs, axis=1), whole, rtol=1e-14, atol=1e-14)
+    for r in range(x.shape[0]):
+        o_r = oracle.ln_proj_forward(x[r:r + 1], lw, lb, W, b, n_proj=4)
+        for p in range(4):
+            # BLAS may block one row differently from many: last-bit differences only
+            np.testing.assert_allclose(o_r[p][0], outs[p][r], rtol=1e-14, atol=1e-14)
+    W2 = np.random.default_rng(4).standard_normal(W.shape)
+    o1 = oracle.ln_proj_forward(x, lw, lb, W, None, n_proj=4)
+    o2 = oracle.ln_proj_forward(x, lw, lb, W2, None, n_proj=4)
+    o3 = oracle.ln_proj_forward(x, lw, lb, 2.0 * W - 3.0 * W2, None, n_proj=4)
+    for p in range(4):
+        np.testing.assert_allclose(o3[p], 2.0 * o1[p] - 3.0 * o2[p], rtol=1e-12, atol=1e-12)
+
+
+def test_three_dim_input():
+    x, lw, lb, W, b = _case(5, R=12)
+    o2 = oracle.ln_proj_forward(x, lw, lb, W, b, n_proj=4)
+    o3 = oracle.ln_proj_forward(x.reshape(3, 4, -1), lw, lb, W, b, n_proj=4)
+    for p in range(4):
+        np.testing.assert_allclose(o3[p].reshape(12, -1), o2[p], rtol=1e-14, atol=1e-14)

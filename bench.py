@@ -106,6 +106,9 @@ def main():
     if args.workload.startswith("ln_"):
         ln_bench(torch, args)
         return
+    if args.workload.startswith("proj_"):
+        proj_bench(torch, args)
+        return
 
     w = W.by_name(args.workload)
     x = W.generate(w)
@@ -351,6 +354,21 @@ def ln_bench(torch, args):
     torch.cuda.synchronize()
     fwd_cold = [l_[0].elapsed_time(l_[1]) for l_ in cev]
     bwd_cold = [l_[2].elapsed_time(l_[3]) for l_ in cev]
+
+    # context: a plain device copy x -> y moves the forward's bytes (read R*C,
+    # write R*C); its time at this size shows what HBM delivers to a kernel
+    # this short, launch and ramp included
+    copy_ms = {}
+    for mode in ("warm", "cold"):
+        ev = [(mk(), mk()) for _ in range(args.steps)]
+        for a, b in ev:
+            if mode == "cold":
+                flush.fill_(3)
+            a.record(stream)
+            y.copy_(xd)
+            b.record(stream)
+        torch.cuda.synchronize()
+        copy_ms[mode] = float(np.median([a.elapsed_time(b) for a, b in ev]))
     del flush
 
     tok = R * C * es
@@ -388,9 +406,116 @@ def ln_bench(torch, args):
                      "fwd_bwd_gbs_median": round(step_bytes / ((np.median(fwd_cold) + np.median(bwd_cold))
                                                                * 1e-3) / 1e9, 1)},
         },
+        "reference_copy": {"note": "torch device copy of x (same bytes as the forward), event-timed median",
+                           "bytes": 2 * tok, "warm_ms": round(copy_ms["warm"], 5),
+                           "cold_ms": round(copy_ms["cold"], 5)},
         "kernels": kernels, "wall_s": round(wall, 3), "roofline": roofline, "cpu_baseline": cpu,
     }
     print(json.dumps(line))
+
+
+def proj_bench(torch, args):
+    """Fused LayerNorm + batched projections (forward) on one of the
+    projection workloads: one step is one evo_ln_proj_fwd over all tokens.
+    `value` is TFLOP/s of the products (2*R*C*P*HD); the roofline is the
+    kernel's HBM bound (its intensity is below the bf16 ridge point)."""
+    from paper_2404_11068_amd import proj as pj
+    from paper_2404_11068_amd import workloads as W
+
+    w = W.proj_by_name(args.workload)
+    d = W.generate_proj(w)
+    bf = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+    x, Wt = bf(d["x"]), bf(d["weight"])
+    lnw, lnb = torch.from_numpy(d["ln_weight"]).cuda(), torch.from_numpy(d["ln_bias"]).cuda()
+    b = None if d["bias"] is None else torch.from_numpy(d["bias"]).cuda()
+    outs = [torch.empty((w.n_rows, w.proj_dim), dtype=torch.bfloat16, device="cuda") for _ in range(w.n_proj)]
+    stream = torch.cuda.current_stream()
+
+    def step():
+        pj.ln_proj_fwd(x, lnw, lnb, Wt, b, n_proj=w.n_proj, eps=w.eps, outs=outs, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    start, stop = mk(), mk()
+    t0 = time.perf_counter()
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = start.elapsed_time(stop) / args.steps
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    res = {}
+    for mode in ("warm", "cold"):
+        ev = [(mk(), mk()) for _ in range(args.steps)]
+        for a, b_ in ev:
+            a.record(stream)
+            b_.record(stream)
+        torch.cuda.synchronize()
+        for a, b_ in ev:
+            if mode == "cold":
+                flush.fill_(1)
+            a.record(stream)
+            step()
+            b_.record(stream)
+        torch.cuda.synchronize()
+        res[mode] = [a.elapsed_time(b_) for a, b_ in ev]
+    del flush
+    k_ms = float(np.mean(res["warm"]))
+    nbytes = w.bytes()
+    ach = nbytes / (k_ms * 1e-3) / 1e9
+    flops = w.flops()
+    roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": measured_traffic("ln_proj_kernel", w.name),
+                "kernel": "ln_proj_kernel", "avg_ms": round(k_ms, 5), "algorithmic_bytes": int(nbytes),
+                "flops": flops, "intensity_flop_per_byte": round(flops / nbytes, 1),
+                "mfma_frac": round(flops / (k_ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)}
+    cpu = None if args.no_cpu_baseline else proj_cpu_baseline(w, d, args.cpu_seconds)
+    line = {
+        "metric": "Fused LayerNorm + batched q/k/v/gate projections, TFLOP/s on 1 MI355X",
+        "value": round(flops / (ms_step * 1e-3) / 1e12, 2), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "n_rows": w.n_rows, "c_in": w.c_in, "n_proj": w.n_proj,
+                   "proj_dim": w.proj_dim, "bias": w.bias, "parallelism": "single-gpu"},
+        "gbs": round(nbytes / (ms_step * 1e-3) / 1e9, 1),
+        "timing": {"warm": {"note": "calls back to back", "ms": _pct(res["warm"])},
+                   "cold": {"note": "512 MiB scratch written before each call, outside the events",
+                            "ms": _pct(res["cold"])}},
+        "wall_s": round(wall, 3), "roofline": roofline, "cpu_baseline": cpu,
+    }
+    print(json.dumps(line))
+
+
+def proj_cpu_baseline(w, d, target_s: float):
+    """The fp64 oracle (LayerNorm + one numpy matmul per projection) on the
+    host, on a slice of rows sized for about target_s."""
+    import oracle
+    from paper_2404_11068_amd import workloads as W
+
+    xf = W.as_float64(d["x"], "bf16")
+    Wf = W.as_float64(d["weight"], "bf16")
+
+    def run(rows):
+        t0 = time.perf_counter()
+        oracle.ln_proj_forward(xf[:rows], d["ln_weight"], d["ln_bias"], Wf, d["bias"], n_proj=w.n_proj, eps=w.eps)
+        return time.perf_counter() - t0
+
+    rows = min(w.n_rows, 4096)
+    t = run(rows)
+    rows = int(max(1, min(w.n_rows, rows * target_s / max(t, 1e-3))))
+    reps = 1
+    t = run(rows)
+    if rows == w.n_rows and t < target_s:
+        reps = max(1, int(target_s / max(t, 1e-3)))
+        t = float(np.median([run(rows) for _ in range(reps)]))
+    return {"value": round(w.flops() * rows / w.n_rows / t / 1e12, 6), "unit": "TFLOP/s",
+            "cores": oracle.threads(), "kind": "oracle", "cpu_model": _cpu_model(),
+            "seconds_per_run": round(t, 4), "runs": reps,
+            "sample": "%d of %d rows, LayerNorm (C, OpenMP) + numpy fp64 matmuls" % (rows, w.n_rows)}
 
 
 def ln_cpu_baseline(w, x, target_s: float):
@@ -449,10 +574,13 @@ def measured_traffic(kernel: str, workload: str):
 # device sources of each kernel family (a change to any of them invalidates
 # the family's recorded counters)
 KERNEL_SOURCES = {"attn": ("evo_frag.h", "evo_fwd.hip", "evo_bwd.hip"),
-                  "ln": ("evo_frag.h", "evo_ln.hip")}
+                  "ln": ("evo_frag.h", "evo_ln.hip"),
+                  "proj": ("evo_frag.h", "evo_proj.hip")}
 
 
 def kernel_family(kernel: str) -> str:
+    if kernel.startswith("ln_proj"):
+        return "proj"
     return "ln" if kernel.startswith("ln_") else "attn"
 
 

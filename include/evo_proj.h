@@ -1,0 +1,63 @@
+/*
+ * evo_proj.h -- C ABI of the fused LayerNorm + batched projections (gfx950).
+ *
+ * The step in front of every Evoformer attention: normalise the input
+ * representation and project it to queries, keys, values and gate logits.
+ * ScaleFold (arXiv 2404.11068), Section 3.3: the four linear layers have no
+ * dependency on each other, so they run as one batched product ("GEMM
+ * Batching"), fused with the LayerNorm that precedes them.  Computed here:
+ *
+ *   y        = LayerNorm(x) over the last axis (as in evo_layernorm.h), bf16
+ *   out_p    = y @ weight[p*HD : (p+1)*HD, :]^T + bias[p*HD : (p+1)*HD]
+ *              for p = 0 .. n_proj-1
+ *
+ * Each out_p is written straight into the attention's token layout: a
+ * contiguous [R, HD] bf16 tensor is the [N, L, H, d] tensor with R = N*L and
+ * HD = H*d, ready for evo_attn_fwd.
+ *
+ * Conventions (dtype and status codes from evo_attn.h):
+ * - Device pointers owned by the caller; nothing is allocated or
+ *   synchronised; the call enqueues one kernel on `stream` and returns.
+ * - x: contiguous [R, C] bf16, 16-byte aligned.  ln_weight, ln_bias: fp32
+ *   [C].  weight: contiguous [n_proj*HD, C] bf16 (torch Linear layout,
+ *   projections stacked), 16-byte aligned.  bias: fp32 [n_proj*HD] or NULL.
+ *   outs: HOST array of n_proj device pointers, each a contiguous [R, HD]
+ *   bf16 tensor, 16-byte aligned, not aliasing each other or any input.
+ *   mean, rstd: fp32 [R] LayerNorm statistics (both or neither; NULL = not
+ *   stored).
+ * - The LayerNorm output is rounded to bf16 before the products (the MFMA
+ *   input precision); products accumulate in fp32; outputs are rounded to
+ *   nearest even.
+ * - Validation happens before any HIP call; errors enqueue nothing.
+ */
+#ifndef EVO_PROJ_H
+#define EVO_PROJ_H
+
+#include "evo_attn.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Compiled set: dtype EVO_DTYPE_BF16; c_in in {64, 128, 256}; proj_dim a
+ * multiple of 32 in [32, 1024]; n_proj in [1, 4]. */
+typedef struct evo_proj_dims {
+    int32_t dtype;     /* EVO_DTYPE_BF16 */
+    int32_t c_in;      /* C */
+    int32_t n_proj;    /* P */
+    int32_t proj_dim;  /* HD = H * d per projection */
+    int64_t n_rows;    /* R >= 0 tokens (N * L) */
+    float eps;         /* LayerNorm epsilon, >= 0 and finite */
+    int32_t reserved;  /* must be 0 */
+} evo_proj_dims;
+
+/* R == 0 validates and returns EVO_OK without touching any pointer. */
+int evo_ln_proj_fwd(const evo_proj_dims *dims, const void *x, const float *ln_weight,
+                    const float *ln_bias, const void *weight, const float *bias,
+                    void *const *outs, float *mean, float *rstd, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EVO_PROJ_H */

@@ -88,4 +88,20 @@ size_t ln_bwd_workspace(const LnProblem &p);
 hipError_t launch_ln_fwd(const LnProblem &p, const LnPtrs &x, hipStream_t s);
 hipError_t launch_ln_bwd(const LnProblem &p, const LnBwdPtrs &x, void *ws, hipStream_t s, Tracer *tr = nullptr);
 
+// LayerNorm + P batched projections (bf16): out_p = LN(x) W_p^T + b_p
+struct PjArgs {
+    const void *x;            // [R, C] bf16
+    const float *lnw, *lnb;   // [C]
+    const void *W;            // [P*HD, C] bf16
+    const float *bias;        // [P*HD] or null
+    void *out0, *out1, *out2, *out3;  // [R, HD] bf16 each (first P used)
+    float *mean, *rstd;       // [R] or null (both or neither)
+    int64_t R;
+    int C, HD, P;
+    float eps;
+};
+
+bool proj_supported(int C, int HD, int P);
+hipError_t launch_ln_proj(const PjArgs &a, hipStream_t s);
+
 }  // namespace evo

@@ -133,7 +133,8 @@ __global__ __launch_bounds__(64 * kLnWaves) void ln_fwd_kernel(const void *__res
     using G = LnGeom<T, C>;
     constexpr int VEC = G::VEC, NV = G::NV, U = G::U;
     constexpr uint32_t rbytes = (uint32_t)C * G::ES;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: scalar addressing
     const int li = lane % G::LPR, rs = lane / G::LPR;
     const int64_t n_pass = (R + G::ROWS - 1) / G::ROWS;
     const int64_t stride = (int64_t)gridDim.x * kLnWaves;
@@ -224,7 +225,8 @@ __global__ __launch_bounds__(64 * kLnWaves) void ln_bwd_kernel(const void *__res
     constexpr int VEC = G::VEC, NV = G::NV, U = G::U;
     constexpr uint32_t rbytes = (uint32_t)C * G::ES;
     __shared__ float red[kLnWaves][2 * C];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: scalar addressing
     const int li = lane % G::LPR, rs = lane / G::LPR;
     constexpr float inv_c = 1.0f / (float)C;
     const int64_t n_pass = (R + G::ROWS - 1) / G::ROWS;

@@ -1,0 +1,63 @@
+// evo_proj_api.cpp -- the C ABI declared in include/evo_proj.h: validation
+// (before any HIP call) and dispatch.
+#include "evo_proj.h"
+
+#include <hip/hip_runtime.h>
+#include <math.h>
+
+#include "evo_kernels.h"
+
+namespace {
+
+bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+int evo_ln_proj_fwd(const evo_proj_dims *d, const void *x, const float *ln_weight, const float *ln_bias,
+                    const void *weight, const float *bias, void *const *outs, float *mean, float *rstd,
+                    void *stream) {
+    if (!d || d->reserved != 0) return EVO_ERR_INVALID_ARG;
+    if (d->dtype != EVO_DTYPE_BF16) return EVO_ERR_UNSUPPORTED;
+    if (d->n_rows < 0 || d->c_in < 1 || d->n_proj < 1 || d->proj_dim < 1 || !(d->eps >= 0.0f) ||
+        !isfinite(d->eps))
+        return EVO_ERR_INVALID_ARG;
+    if (!evo::proj_supported(d->c_in, d->proj_dim, d->n_proj)) return EVO_ERR_UNSUPPORTED;
+    // the kernels address one workgroup's rows with 32-bit offsets; the grid is 32-bit
+    if (d->n_rows > (int64_t(1) << 36)) return EVO_ERR_UNSUPPORTED;
+    if (d->n_rows == 0) return EVO_OK;
+    if (!x || !ln_weight || !ln_bias || !weight || !outs) return EVO_ERR_INVALID_ARG;
+    if ((mean == nullptr) != (rstd == nullptr) || (mean && (void *)mean == (void *)rstd)) return EVO_ERR_INVALID_ARG;
+    for (int p = 0; p < d->n_proj; ++p) {
+        if (!outs[p] || outs[p] == x || outs[p] == weight) return EVO_ERR_INVALID_ARG;
+        for (int q = 0; q < p; ++q)
+            if (outs[q] == outs[p]) return EVO_ERR_INVALID_ARG;
+        if (!aligned(outs[p], 16)) return EVO_ERR_ALIGNMENT;
+    }
+    if (!aligned(x, 16) || !aligned(weight, 16) || !aligned(ln_weight, 16) || !aligned(ln_bias, 16) ||
+        (bias && !aligned(bias, 16)) || (mean && (!aligned(mean, 4) || !aligned(rstd, 4))))
+        return EVO_ERR_ALIGNMENT;
+    evo::PjArgs a{};
+    a.x = x;
+    a.lnw = ln_weight;
+    a.lnb = ln_bias;
+    a.W = weight;
+    a.bias = bias;
+    void *o[4] = {outs[0], d->n_proj > 1 ? outs[1] : nullptr, d->n_proj > 2 ? outs[2] : nullptr,
+                  d->n_proj > 3 ? outs[3] : nullptr};
+    a.out0 = o[0];
+    a.out1 = o[1];
+    a.out2 = o[2];
+    a.out3 = o[3];
+    a.mean = mean;
+    a.rstd = rstd;
+    a.R = d->n_rows;
+    a.C = d->c_in;
+    a.HD = d->proj_dim;
+    a.P = d->n_proj;
+    a.eps = d->eps;
+    return evo::launch_ln_proj(a, (hipStream_t)stream) == hipSuccess ? EVO_OK : EVO_ERR_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,77 @@
+"""Python binding of the C ABI in include/evo_proj.h (argument marshalling only).
+
+The fused LayerNorm + batched projections run in ``libevoattn.so``; this
+module passes torch tensors' device pointers and raises on a nonzero status.
+No fallback exists.
+
+  x : contiguous [..., C] bf16
+  ln_weight, ln_bias : fp32 [C]
+  weight : contiguous [n_proj * HD, C] bf16 (torch Linear layout, projections stacked)
+  bias : fp32 [n_proj * HD] or None
+  returns n_proj tensors [..., HD] bf16 (view them as [..., H, d] for the attention)
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import List, Optional
+
+import torch
+
+from .evo_attn import EvoAttnError, _ptr, _stream, load_library, EVO_DTYPE_BF16
+
+
+class evo_proj_dims(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int32), ("c_in", ctypes.c_int32), ("n_proj", ctypes.c_int32),
+                ("proj_dim", ctypes.c_int32), ("n_rows", ctypes.c_int64), ("eps", ctypes.c_float),
+                ("reserved", ctypes.c_int32)]
+
+
+_bound = False
+
+
+def _lib():
+    global _bound
+    lib = load_library()
+    if not _bound:
+        P = ctypes.c_void_p
+        lib.evo_ln_proj_fwd.argtypes = [ctypes.POINTER(evo_proj_dims), P, P, P, P, P, ctypes.POINTER(P), P, P, P]
+        lib.evo_ln_proj_fwd.restype = ctypes.c_int
+        _bound = True
+    return lib
+
+
+def ln_proj_fwd(x: torch.Tensor, ln_weight: torch.Tensor, ln_bias: torch.Tensor, weight: torch.Tensor,
+                bias: Optional[torch.Tensor] = None, n_proj: int = 4, eps: float = 1e-5, *,
+                outs: Optional[List[torch.Tensor]] = None, mean=None, rstd=None, need_stats: bool = False,
+                stream=None) -> List[torch.Tensor]:
+    """outs[p] = LayerNorm(x) @ weight[p*HD:(p+1)*HD].T + bias[p*HD:(p+1)*HD].
+
+    With need_stats (or mean/rstd given) the LayerNorm statistics are stored
+    too and returned after the outputs: (outs, mean, rstd)."""
+    lib = _lib()
+    if x.dtype != torch.bfloat16 or weight.dtype != torch.bfloat16:
+        raise ValueError("x and weight must be bfloat16")
+    if not x.is_contiguous() or not weight.is_contiguous() or weight.dim() != 2:
+        raise ValueError("x and weight must be contiguous; weight is [n_proj*HD, C]")
+    C = x.shape[-1]
+    if weight.shape[1] != C or weight.shape[0] % n_proj:
+        raise ValueError("weight must be [n_proj*HD, C]")
+    HD = weight.shape[0] // n_proj
+    R = x.numel() // C if C else 0
+    if outs is None:
+        outs = [torch.empty(x.shape[:-1] + (HD,), dtype=torch.bfloat16, device=x.device) for _ in range(n_proj)]
+    if len(outs) != n_proj or any(o.dtype != torch.bfloat16 or not o.is_contiguous() or o.numel() != R * HD
+                                  for o in outs):
+        raise ValueError("outs must be n_proj contiguous bf16 tensors of R*HD elements")
+    if need_stats or mean is not None:
+        mean = torch.empty(x.shape[:-1], dtype=torch.float32, device=x.device) if mean is None else mean
+        rstd = torch.empty(x.shape[:-1], dtype=torch.float32, device=x.device) if rstd is None else rstd
+    d = evo_proj_dims(EVO_DTYPE_BF16, C, n_proj, HD, R, float(eps), 0)
+    ptrs = (ctypes.c_void_p * n_proj)(*[ctypes.c_void_p(o.data_ptr()) for o in outs])
+    st = lib.evo_ln_proj_fwd(ctypes.byref(d), _ptr(x), _ptr(ln_weight), _ptr(ln_bias), _ptr(weight), _ptr(bias),
+                             ptrs, _ptr(mean), _ptr(rstd), _stream(stream))
+    if st:
+        raise EvoAttnError(st, "evo_ln_proj_fwd")
+    if mean is not None:
+        return outs, mean, rstd
+    return outs

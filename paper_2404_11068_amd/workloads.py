@@ -229,3 +229,67 @@ def generate_ln(w: LnWorkload, seed: Optional[int] = None, n_rows: Optional[int]
     bias = (0.2 * rng.standard_normal(C)).astype(np.float32)
     dy = rng.standard_normal((R, C))
     return {"x": _store(x, w.dtype), "weight": weight, "bias": bias, "dy": _store(dy, w.dtype)}
+
+
+# ---------------------------------------------------------------------------
+# Fused LayerNorm + batched projections: the input side of each attention
+# (ScaleFold Section 3.3, "GEMM Batching": query, key, value and gate linear
+# layers over one normalised input).  Shapes of the three attention inputs at
+# the 256-residue crop.  Weights ~ N(0, 1/C) (LeCun-normal scale), biases
+# ~ N(0, 0.1^2), LayerNorm parameters near the identity.
+# Draw order: row offset, row spread, x, ln weight, ln bias, weight, bias.
+
+@dataclasses.dataclass(frozen=True)
+class ProjWorkload:
+    name: str
+    n_rows: int      # R = N * L tokens
+    c_in: int        # C
+    proj_dim: int    # HD = H * d
+    n_proj: int = 4
+    bias: bool = True
+    eps: float = 1e-5
+    seed: int = 0
+    description: str = ""
+
+    def flops(self) -> float:
+        return 2.0 * self.n_rows * self.c_in * self.n_proj * self.proj_dim
+
+    def bytes(self) -> int:
+        # x in, P outputs out (bf16), weight and parameters in
+        return (2 * self.n_rows * self.c_in + 2 * self.n_rows * self.n_proj * self.proj_dim
+                + 2 * self.n_proj * self.proj_dim * self.c_in + 8 * self.c_in
+                + (4 * self.n_proj * self.proj_dim if self.bias else 0))
+
+
+PROJ_WORKLOADS = [
+    ProjWorkload("proj_msa_bf16", 128 * 256, 256, 8 * 32, seed=3001,
+                 description="MSA row/column attention input: 128 x 256 tokens, c_m = 256 -> q,k,v,g [H=8, d=32]"),
+    ProjWorkload("proj_tri_bf16", 256 * 256, 128, 4 * 32, seed=3002,
+                 description="triangle attention input: 256 x 256 pairs, c_z = 128 -> q,k,v,g [H=4, d=32]"),
+    ProjWorkload("proj_extra_msa_bf16", 1024 * 256, 64, 8 * 8, seed=3003,
+                 description="extra-MSA attention input: 1024 x 256 tokens, c_e = 64 -> q,k,v,g [H=8, d=8]"),
+]
+
+
+def proj_by_name(name: str) -> ProjWorkload:
+    for w in PROJ_WORKLOADS:
+        if w.name == name:
+            return w
+    raise KeyError(name)
+
+
+def generate_proj(w: ProjWorkload, seed: Optional[int] = None, n_rows: Optional[int] = None
+                  ) -> Dict[str, np.ndarray]:
+    """x [R, C] and weight [P*HD, C] as bf16 bits; ln_weight, ln_bias [C] and
+    bias [P*HD] (or None) as fp32."""
+    rng = np.random.Generator(np.random.PCG64(w.seed if seed is None else seed))
+    R = w.n_rows if n_rows is None else n_rows
+    C, F = w.c_in, w.n_proj * w.proj_dim
+    offset = rng.standard_normal((R, 1)) * 2.0
+    spread = rng.uniform(0.25, 4.0, size=(R, 1))
+    x = rng.standard_normal((R, C)) * spread + offset
+    lnw = (1.0 + 0.2 * rng.standard_normal(C)).astype(np.float32)
+    lnb = (0.2 * rng.standard_normal(C)).astype(np.float32)
+    W = rng.standard_normal((F, C)) / math.sqrt(C)
+    b = (0.1 * rng.standard_normal(F)).astype(np.float32) if w.bias else None
+    return {"x": _store(x, "bf16"), "ln_weight": lnw, "ln_bias": lnb, "weight": _store(W, "bf16"), "bias": b}

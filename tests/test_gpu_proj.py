@@ -1,0 +1,109 @@
+"""GPU parity of the fused LayerNorm + batched projections (through the C ABI)
+against the fp64 oracle (LayerNorm then one matmul per projection).
+
+* every projection workload at full size, all outputs, all elements;
+* every compiled input width with ragged token counts, several projection
+  widths and counts, with and without bias and statistics;
+* the outputs feed the attention directly ([R, HD] == [N, L, H, d]).
+
+Tolerance (bf16 outputs): |x - ref| <= 1e-2 + 1e-2 |ref| element-wise and
+||x - ref|| <= 5e-3 ||ref||.  The kernel rounds the normalised input to bf16
+before the products (relative 2^-9 per element, about 2e-3 of the output
+norm after the sum over C) and rounds the outputs once more (2^-9); 5e-3
+leaves room for both and still fails on any real slip.
+Statistics: as for the stand-alone LayerNorm (rtol 1e-5).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2404_11068_amd import proj as pj
+from paper_2404_11068_amd import workloads as W
+from tests.parity_util import to_device, to_f64
+
+pytestmark = pytest.mark.gpu
+
+
+def _check(name, got, ref, atol=1e-2, rtol=1e-2, norm=5e-3):
+    assert got.shape == ref.shape, (name, got.shape, ref.shape)
+    assert np.isfinite(got).all(), name
+    err = np.abs(got - ref)
+    bound = atol + rtol * np.abs(ref)
+    i = int(np.argmax(err - bound))
+    assert (err <= bound).all(), (name, "max err %.3g at ref %.3g" % (err.flat[i], ref.flat[i]))
+    rel = np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-30)
+    assert rel <= norm, (name, "normwise rel err %.3g" % rel)
+    return rel
+
+
+def run_case(w, d, label, stats=True):
+    print("\n[case]", label, flush=True)
+    x = to_device(d["x"], "bf16")
+    Wt = to_device(d["weight"], "bf16")
+    lnw, lnb = torch.from_numpy(d["ln_weight"]).cuda(), torch.from_numpy(d["ln_bias"]).cuda()
+    b = None if d["bias"] is None else torch.from_numpy(d["bias"]).cuda()
+    res = pj.ln_proj_fwd(x, lnw, lnb, Wt, b, n_proj=w.n_proj, eps=w.eps, need_stats=stats)
+    outs, mean, rstd = res if stats else (res, None, None)
+    torch.cuda.synchronize()
+    xf = W.as_float64(d["x"], "bf16")
+    ref = oracle.ln_proj_forward(xf, d["ln_weight"], d["ln_bias"], W.as_float64(d["weight"], "bf16"),
+                                 d["bias"], n_proj=w.n_proj, eps=w.eps)
+    worst = 0.0
+    for p in range(w.n_proj):
+        worst = max(worst, _check("%s out%d" % (label, p), to_f64(outs[p]), ref[p]))
+    if stats:
+        _, rm, rr = oracle.layernorm_forward(xf, None, None, w.eps)
+        np.testing.assert_allclose(to_f64(mean), rm, rtol=1e-5, atol=1e-5 * max(np.abs(xf).max(), 1.0))
+        np.testing.assert_allclose(to_f64(rstd), rr, rtol=1e-5)
+    print("  worst normwise rel err %.2e" % worst, flush=True)
+
+
+@pytest.mark.parametrize("name", [w.name for w in W.PROJ_WORKLOADS])
+def test_full_workload(name):
+    w = W.proj_by_name(name)
+    run_case(w, W.generate_proj(w), name)
+
+
+CASES = [
+    # R, C, HD, P, bias, stats
+    (1, 64, 32, 1, False, True),
+    (33, 64, 64, 4, True, True),
+    (100, 128, 96, 3, True, False),
+    (1000, 128, 128, 4, False, True),
+    (77, 256, 256, 4, True, True),
+    (513, 256, 32, 2, True, True),
+    (64, 256, 1024, 1, False, False),
+    (129, 64, 160, 4, True, True),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "R%d_C%d_HD%d_P%d_b%d_s%d" % c)
+def test_shapes(case):
+    R, C, HD, P, bias, stats = case
+    w = W.ProjWorkload("adhoc", R, C, HD, n_proj=P, bias=bias, seed=R + C + HD)
+    run_case(w, W.generate_proj(w), str(case), stats=stats)
+
+
+def test_feeds_attention_layout():
+    # q, k, v, g for an MSA-row shaped attention come out as [N, L, H, d]
+    from paper_2404_11068_amd import evo_attn as ea
+    N, L, H, d, C = 4, 64, 8, 32, 256
+    w = W.ProjWorkload("adhoc", N * L, C, H * d, seed=5)
+    dd = W.generate_proj(w)
+    x = to_device(dd["x"], "bf16").view(N, L, C)
+    q, k, v, g = pj.ln_proj_fwd(x, torch.from_numpy(dd["ln_weight"]).cuda(),
+                                torch.from_numpy(dd["ln_bias"]).cuda(), to_device(dd["weight"], "bf16"),
+                                torch.from_numpy(dd["bias"]).cuda(), n_proj=4)
+    assert q.shape == (N, L, H * d)
+    out, lse = ea.evo_attn_fwd(*(t.view(N, L, H, d) for t in (q, k, v, g)))
+    torch.cuda.synchronize()
+    assert torch.isfinite(out.float()).all() and torch.isfinite(lse).all()
+
+
+def test_empty():
+    x = torch.empty((0, 128), dtype=torch.bfloat16, device="cuda")
+    Wt = torch.zeros((4 * 64, 128), dtype=torch.bfloat16, device="cuda")
+    one, zero = torch.ones(128, device="cuda"), torch.zeros(128, device="cuda")
+    outs = pj.ln_proj_fwd(x, one, zero, Wt, None, n_proj=4)
+    assert all(o.shape == (0, 64) for o in outs)

@@ -1,0 +1,76 @@
+"""Host-side checks of evo_ln_proj_fwd (no GPU): the symbol is exported and
+every invalid call is rejected before any HIP call (fake device addresses
+are never dereferenced)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2404_11068_amd import evo_attn as ea
+from paper_2404_11068_amd import proj as pj
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x7f0000000000
+P = lambda x: None if x is None else ctypes.c_void_p(x)
+
+
+def _lib():
+    if not os.path.exists(ea.LIB_PATH):
+        pytest.skip("libevoattn.so not built")
+    return pj._lib()
+
+
+def test_exports_declared_symbol():
+    lib = _lib()
+    decls = re.findall(r"^\s*int\s*(evo_\w+)\s*\(", open(os.path.join(ROOT, "include", "evo_proj.h")).read(),
+                       flags=re.M)
+    assert decls == ["evo_ln_proj_fwd"]
+    assert hasattr(lib, "evo_ln_proj_fwd")
+
+
+def _call(dims, x=FAKE, lnw=FAKE + 0x10000, lnb=FAKE + 0x11000, w=FAKE + 0x20000, b=None,
+          outs=(FAKE + 0x100000, FAKE + 0x200000, FAKE + 0x300000, FAKE + 0x400000), mean=None, rstd=None,
+          n_out=None):
+    lib = _lib()
+    arr = None
+    if outs is not None:
+        n = len(outs) if n_out is None else n_out
+        arr = (ctypes.c_void_p * max(n, 1))(*[ctypes.c_void_p(o) if o is not None else None for o in outs[:n]])
+    return lib.evo_ln_proj_fwd(ctypes.byref(dims) if dims is not None else None, P(x), P(lnw), P(lnb), P(w), P(b),
+                               arr, P(mean), P(rstd), None)
+
+
+def _dims(**kw):
+    d = dict(dtype=1, c_in=128, n_proj=4, proj_dim=128, n_rows=1000, eps=1e-5, reserved=0)
+    d.update(kw)
+    return pj.evo_proj_dims(d["dtype"], d["c_in"], d["n_proj"], d["proj_dim"], d["n_rows"], d["eps"], d["reserved"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=0), 2), (dict(c_in=96), 2), (dict(c_in=512), 2), (dict(proj_dim=48), 2),
+    (dict(proj_dim=2048), 2), (dict(n_proj=5), 2), (dict(n_proj=0), 1), (dict(n_rows=-2), 1),
+    (dict(eps=-1.0), 1), (dict(eps=float("nan")), 1), (dict(reserved=1), 1), (dict(n_rows=1 << 40), 2),
+])
+def test_rejects_bad_dims(kw, status):
+    assert _call(_dims(**kw)) == status
+
+
+def test_rejects_bad_pointers():
+    d = _dims()
+    assert _call(None) == 1
+    for k in ("x", "lnw", "lnb", "w"):
+        assert _call(d, **{k: None}) == 1, k
+    assert _call(d, outs=None) == 1
+    assert _call(d, outs=(FAKE + 0x100000, None, FAKE + 0x300000, FAKE + 0x400000)) == 1
+    assert _call(d, outs=(FAKE + 0x100000, FAKE + 0x100000, FAKE + 0x300000, FAKE + 0x400000)) == 1
+    assert _call(d, outs=(FAKE, FAKE + 0x200000, FAKE + 0x300000, FAKE + 0x400000)) == 1   # aliases x
+    assert _call(d, mean=FAKE + 0x500000) == 1                                             # rstd missing
+    assert _call(d, x=FAKE + 8) == 3
+    assert _call(d, w=FAKE + 0x20004) == 3
+    assert _call(d, b=FAKE + 0x30008) == 3
+    assert _call(d, outs=(FAKE + 0x100008, FAKE + 0x200000, FAKE + 0x300000, FAKE + 0x400000)) == 3
+
+
+def test_empty_needs_no_pointers():
+    assert _call(_dims(n_rows=0), x=None, lnw=None, lnb=None, w=None, outs=None) == 0

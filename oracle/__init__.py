@@ -200,3 +200,24 @@ def ln_proj_forward(x, ln_weight, ln_bias, weight, bias=None, n_proj: int = 1, e
             o = o + _f64(bias)[p * HD:(p + 1) * HD]
         outs.append(o)
     return outs
+
+
+def pair_bias_forward(z, ln_weight, ln_bias, weight, eps: float = 1e-5, transpose: bool = False):
+    """Pair bias of the Evoformer attentions: a LayerNorm of each pair entry
+    followed by a linear map without bias to one value per head (the bias
+    term that ScaleFold Section 3.3 adds to the logits).
+
+    z [B, Li, Lj, C]; weight [H, C].  Returns [B, H, Li, Lj] with
+        out[b, h, i, j] = sum_c LN(z[b, i, j, :])[c] * weight[h, c]
+    or, with transpose, [B, H, Lj, Li] with out[b, h, j, i] equal to the
+    same value (the layout triangle attention around the ending node reads).
+    The contraction is a library primitive (numpy matmul, fp64)."""
+    z = _f64(z)
+    W = _f64(weight)
+    if z.ndim != 4 or W.ndim != 2 or W.shape[1] != z.shape[3]:
+        raise ValueError("z is [B, Li, Lj, C] and weight [H, C]")
+    y, _, _ = layernorm_forward(z, ln_weight, ln_bias, eps)
+    out = np.moveaxis(y @ W.T, 3, 1)          # [B, H, Li, Lj]
+    if transpose:
+        out = np.swapaxes(out, 2, 3)          # [B, H, Lj, Li]
+    return np.ascontiguousarray(out)

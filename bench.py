@@ -109,6 +109,9 @@ def main():
     if args.workload.startswith("proj_"):
         proj_bench(torch, args)
         return
+    if args.workload.startswith("pb_"):
+        pair_bias_bench(torch, args)
+        return
 
     w = W.by_name(args.workload)
     x = W.generate(w)
@@ -490,6 +493,94 @@ def proj_bench(torch, args):
     print(json.dumps(line))
 
 
+def pair_bias_bench(torch, args):
+    """Pair bias (LayerNorm of each pair entry + bias-free projection to the
+    heads, written in the attention's bias layout) on one pair-bias workload.
+    `value` is algorithmic HBM bytes per second (read z, write the bias)."""
+    from paper_2404_11068_amd import proj as pj
+    from paper_2404_11068_amd import workloads as W
+
+    w = W.pair_bias_by_name(args.workload)
+    d = W.generate_pair_bias(w)
+    bf = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+    z, Wt = bf(d["z"]), bf(d["weight"])
+    lnw, lnb = torch.from_numpy(d["ln_weight"]).cuda(), torch.from_numpy(d["ln_bias"]).cuda()
+    L, H = w.seq_len, w.n_heads
+    out = torch.empty((w.n_batch, H, L, L), dtype=torch.bfloat16, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def step():
+        pj.ln_pair_bias_fwd(z, lnw, lnb, Wt, w.eps, w.transpose, out=out, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    start, stop = mk(), mk()
+    t0 = time.perf_counter()
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = start.elapsed_time(stop) / args.steps
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    res = {}
+    for mode in ("warm", "cold"):
+        ev = [(mk(), mk()) for _ in range(args.steps)]
+        for a, b_ in ev:
+            a.record(stream)
+            b_.record(stream)
+        torch.cuda.synchronize()
+        for a, b_ in ev:
+            if mode == "cold":
+                flush.fill_(1)
+            a.record(stream)
+            step()
+            b_.record(stream)
+        torch.cuda.synchronize()
+        res[mode] = [a.elapsed_time(b_) for a, b_ in ev]
+    del flush
+    k_ms = float(np.mean(res["warm"]))
+    nbytes = w.bytes()
+    ach = nbytes / (k_ms * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": measured_traffic("pair_bias_kernel", w.name),
+                "kernel": "pair_bias_kernel", "avg_ms": round(k_ms, 5), "algorithmic_bytes": int(nbytes)}
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        zf, Wf = W.as_float64(d["z"], "bf16"), W.as_float64(d["weight"], "bf16")
+        run = lambda: oracle.pair_bias_forward(zf, d["ln_weight"], d["ln_bias"], Wf, w.eps, w.transpose)
+        t1 = time.perf_counter()
+        run()
+        t = time.perf_counter() - t1
+        reps = max(1, int(args.cpu_seconds / max(t, 1e-3)))
+        ts = []
+        for _ in range(reps):
+            t1 = time.perf_counter()
+            run()
+            ts.append(time.perf_counter() - t1)
+        t = float(np.median(ts))
+        cpu = {"value": round(nbytes / t / 1e9, 3), "unit": "GB/s", "cores": oracle.threads(), "kind": "oracle",
+               "cpu_model": _cpu_model(), "seconds_per_run": round(t, 4), "runs": reps,
+               "sample": "whole workload, LayerNorm (C, OpenMP) + numpy fp64 matmul, median of %d runs" % reps}
+    line = {
+        "metric": "Pair bias (LayerNorm + projection to heads, attention layout), GB/s on 1 MI355X",
+        "value": round(nbytes / (ms_step * 1e-3) / 1e9, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "n_batch": w.n_batch, "seq_len": L, "c_in": w.c_in, "n_heads": H,
+                   "transpose": w.transpose, "parallelism": "single-gpu"},
+        "timing": {"warm": {"note": "calls back to back", "ms": _pct(res["warm"])},
+                   "cold": {"note": "512 MiB scratch written before each call, outside the events",
+                            "ms": _pct(res["cold"])}},
+        "wall_s": round(wall, 3), "roofline": roofline, "cpu_baseline": cpu,
+    }
+    print(json.dumps(line))
+
+
 def proj_cpu_baseline(w, d, target_s: float):
     """The fp64 oracle (LayerNorm + one numpy matmul per projection) on the
     host, on a slice of rows sized for about target_s."""
@@ -575,12 +666,15 @@ def measured_traffic(kernel: str, workload: str):
 # the family's recorded counters)
 KERNEL_SOURCES = {"attn": ("evo_frag.h", "evo_fwd.hip", "evo_bwd.hip"),
                   "ln": ("evo_frag.h", "evo_ln.hip"),
-                  "proj": ("evo_frag.h", "evo_proj.hip")}
+                  "proj": ("evo_frag.h", "evo_proj.hip"),
+                  "pb": ("evo_frag.h", "evo_pair_bias.hip")}
 
 
 def kernel_family(kernel: str) -> str:
     if kernel.startswith("ln_proj"):
         return "proj"
+    if kernel.startswith("pair_bias"):
+        return "pb"
     return "ln" if kernel.startswith("ln_") else "attn"
 
 

@@ -56,6 +56,44 @@ int evo_ln_proj_fwd(const evo_proj_dims *dims, const void *x, const float *ln_we
                     const float *ln_bias, const void *weight, const float *bias,
                     void *const *outs, float *mean, float *rstd, void *stream);
 
+/*
+ * Pair bias: the logit bias every pair-biased Evoformer attention adds before
+ * its softmax (ScaleFold Section 3.3, "Multi Head Attention"), a LayerNorm of
+ * each pair entry followed by a bias-free linear map to one value per head,
+ * written straight into the [B, H, L, L] layout evo_attn_fwd reads:
+ *
+ *   y          = LayerNorm(z[b, i, j, :])   (fp32 statistics, rounded to bf16)
+ *   v[h]       = sum_c y[c] * weight[h, c]  (fp32 accumulation)
+ *   transpose == 0:  out[b, h, i, j] = v[h]        out is [B, H, Li, Lj]
+ *   transpose == 1:  out[b, h, j, i] = v[h]        out is [B, H, Lj, Li]
+ *
+ * (the transposed layout is the bias of triangle attention around the ending
+ * node, which attends over the transposed pair representation).
+ *
+ * z: contiguous [B, Li, Lj, C] bf16, 16-byte aligned; ln_weight, ln_bias:
+ * fp32 [C], 16-byte aligned; weight: contiguous [H, C] bf16, 16-byte aligned;
+ * out: contiguous bf16 (shape above), 16-byte aligned, not aliasing z;
+ * mean, rstd: fp32 [B, Li, Lj] (both or neither).
+ * Compiled set: C in {64, 128, 256}; H in {1, 2, 4, 8, 16}; Li and Lj
+ * multiples of 8 with H * Li * Lj * 2 bytes below 2^31.  B, Li or Lj == 0
+ * validates and returns EVO_OK without touching any pointer.
+ */
+typedef struct evo_pair_bias_dims {
+    int32_t dtype;      /* EVO_DTYPE_BF16 */
+    int32_t c_in;       /* C */
+    int32_t n_heads;    /* H */
+    int32_t transpose;  /* 0 or 1, see above */
+    int64_t n_batch;    /* B >= 0 */
+    int64_t len_i;      /* Li >= 0 */
+    int64_t len_j;      /* Lj >= 0 */
+    float eps;          /* >= 0 and finite */
+    int32_t reserved;   /* must be 0 */
+} evo_pair_bias_dims;
+
+int evo_ln_pair_bias_fwd(const evo_pair_bias_dims *dims, const void *z, const float *ln_weight,
+                         const float *ln_bias, const void *weight, void *out, float *mean, float *rstd,
+                         void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -101,6 +101,21 @@ struct PjArgs {
     float eps;
 };
 
+// LayerNorm of pair entries projected to per-head logit biases (bf16)
+struct PbArgs {
+    const void *z;            // [B, Li, Lj, C] bf16
+    const float *lnw, *lnb;   // [C]
+    const void *W;            // [H, C] bf16
+    void *out;                // [B, H, Li, Lj] (or [B, H, Lj, Li] when transpose) bf16
+    float *mean, *rstd;       // [B, Li, Lj] or null (both or neither)
+    int64_t B;
+    int Li, Lj, C, H, transpose;
+    float eps;
+};
+
+bool pair_bias_supported(int C, int H);
+hipError_t launch_pair_bias(const PbArgs &a, hipStream_t s);
+
 bool proj_supported(int C, int HD, int P);
 hipError_t launch_ln_proj(const PjArgs &a, hipStream_t s);
 

@@ -60,4 +60,40 @@ int evo_ln_proj_fwd(const evo_proj_dims *d, const void *x, const float *ln_weigh
     return evo::launch_ln_proj(a, (hipStream_t)stream) == hipSuccess ? EVO_OK : EVO_ERR_HIP;
 }
 
+int evo_ln_pair_bias_fwd(const evo_pair_bias_dims *d, const void *z, const float *ln_weight, const float *ln_bias,
+                         const void *weight, void *out, float *mean, float *rstd, void *stream) {
+    if (!d || d->reserved != 0) return EVO_ERR_INVALID_ARG;
+    if (d->dtype != EVO_DTYPE_BF16) return EVO_ERR_UNSUPPORTED;
+    if (d->n_batch < 0 || d->len_i < 0 || d->len_j < 0 || d->c_in < 1 || d->n_heads < 1 ||
+        (d->transpose != 0 && d->transpose != 1) || !(d->eps >= 0.0f) || !isfinite(d->eps))
+        return EVO_ERR_INVALID_ARG;
+    if (!evo::pair_bias_supported(d->c_in, d->n_heads)) return EVO_ERR_UNSUPPORTED;
+    if (d->len_i % 8 != 0 || d->len_j % 8 != 0) return EVO_ERR_UNSUPPORTED;
+    if ((int64_t)d->n_heads * d->len_i * d->len_j * 2 >= 0x7fffffffLL ||
+        d->len_j * d->c_in * 2 >= 0x7fffffffLL || d->n_batch > 65535)
+        return EVO_ERR_UNSUPPORTED;
+    if (d->n_batch == 0 || d->len_i == 0 || d->len_j == 0) return EVO_OK;
+    if (!z || !ln_weight || !ln_bias || !weight || !out || out == z) return EVO_ERR_INVALID_ARG;
+    if ((mean == nullptr) != (rstd == nullptr) || (mean && (void *)mean == (void *)rstd)) return EVO_ERR_INVALID_ARG;
+    if (!aligned(z, 16) || !aligned(weight, 16) || !aligned(out, 16) || !aligned(ln_weight, 16) ||
+        !aligned(ln_bias, 16) || (mean && (!aligned(mean, 4) || !aligned(rstd, 4))))
+        return EVO_ERR_ALIGNMENT;
+    evo::PbArgs a{};
+    a.z = z;
+    a.lnw = ln_weight;
+    a.lnb = ln_bias;
+    a.W = weight;
+    a.out = out;
+    a.mean = mean;
+    a.rstd = rstd;
+    a.B = d->n_batch;
+    a.Li = (int)d->len_i;
+    a.Lj = (int)d->len_j;
+    a.C = d->c_in;
+    a.H = d->n_heads;
+    a.transpose = d->transpose;
+    a.eps = d->eps;
+    return evo::launch_pair_bias(a, (hipStream_t)stream) == hipSuccess ? EVO_OK : EVO_ERR_HIP;
+}
+
 }  // extern "C"

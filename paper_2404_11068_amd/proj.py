@@ -75,3 +75,57 @@ def ln_proj_fwd(x: torch.Tensor, ln_weight: torch.Tensor, ln_bias: torch.Tensor,
     if mean is not None:
         return outs, mean, rstd
     return outs
+
+
+class evo_pair_bias_dims(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int32), ("c_in", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("transpose", ctypes.c_int32), ("n_batch", ctypes.c_int64), ("len_i", ctypes.c_int64),
+                ("len_j", ctypes.c_int64), ("eps", ctypes.c_float), ("reserved", ctypes.c_int32)]
+
+
+_pb_bound = False
+
+
+def _pb_lib():
+    global _pb_bound
+    lib = load_library()
+    if not _pb_bound:
+        P = ctypes.c_void_p
+        lib.evo_ln_pair_bias_fwd.argtypes = [ctypes.POINTER(evo_pair_bias_dims)] + [P] * 8
+        lib.evo_ln_pair_bias_fwd.restype = ctypes.c_int
+        _pb_bound = True
+    return lib
+
+
+def ln_pair_bias_fwd(z: torch.Tensor, ln_weight: torch.Tensor, ln_bias: torch.Tensor, weight: torch.Tensor,
+                     eps: float = 1e-5, transpose: bool = False, *, out: Optional[torch.Tensor] = None,
+                     need_stats: bool = False, stream=None):
+    """Pair bias [B, H, Li, Lj] (or [B, H, Lj, Li] with transpose) from the
+    pair representation z [B, Li, Lj, C]: LayerNorm of each entry, then a
+    bias-free linear map with weight [H, C].  With need_stats also returns
+    the LayerNorm mean and rstd [B, Li, Lj]."""
+    lib = _pb_lib()
+    if z.dim() == 3:
+        z = z.unsqueeze(0)
+    if z.dtype != torch.bfloat16 or weight.dtype != torch.bfloat16 or not z.is_contiguous() \
+            or not weight.is_contiguous():
+        raise ValueError("z and weight must be contiguous bfloat16")
+    B, Li, Lj, C = z.shape
+    H = weight.shape[0]
+    if weight.shape != (H, C):
+        raise ValueError("weight must be [H, C]")
+    shape = (B, H, Lj, Li) if transpose else (B, H, Li, Lj)
+    if out is None:
+        out = torch.empty(shape, dtype=torch.bfloat16, device=z.device)
+    if tuple(out.shape) != shape or out.dtype != torch.bfloat16 or not out.is_contiguous():
+        raise ValueError("out must be a contiguous bf16 tensor of shape %s" % (shape,))
+    mean = rstd = None
+    if need_stats:
+        mean = torch.empty((B, Li, Lj), dtype=torch.float32, device=z.device)
+        rstd = torch.empty((B, Li, Lj), dtype=torch.float32, device=z.device)
+    d = evo_pair_bias_dims(EVO_DTYPE_BF16, C, H, 1 if transpose else 0, B, Li, Lj, float(eps), 0)
+    st = lib.evo_ln_pair_bias_fwd(ctypes.byref(d), _ptr(z), _ptr(ln_weight), _ptr(ln_bias), _ptr(weight),
+                                  _ptr(out), _ptr(mean), _ptr(rstd), _stream(stream))
+    if st:
+        raise EvoAttnError(st, "evo_ln_pair_bias_fwd")
+    return (out, mean, rstd) if need_stats else out

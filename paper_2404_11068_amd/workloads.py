@@ -293,3 +293,55 @@ def generate_proj(w: ProjWorkload, seed: Optional[int] = None, n_rows: Optional[
     W = rng.standard_normal((F, C)) / math.sqrt(C)
     b = (0.1 * rng.standard_normal(F)).astype(np.float32) if w.bias else None
     return {"x": _store(x, "bf16"), "ln_weight": lnw, "ln_bias": lnb, "weight": _store(W, "bf16"), "bias": b}
+
+
+# ---------------------------------------------------------------------------
+# Pair bias: LayerNorm(z) -> H logit biases per residue pair at the 256 crop
+# (c_z = 128).  Weights ~ N(0, 1/C); the rest as in the other generators.
+# Draw order: entry offset, entry spread, z, ln weight, ln bias, weight.
+
+@dataclasses.dataclass(frozen=True)
+class PairBiasWorkload:
+    name: str
+    n_batch: int
+    seq_len: int
+    c_in: int
+    n_heads: int
+    transpose: bool = False
+    eps: float = 1e-5
+    seed: int = 0
+    description: str = ""
+
+    def bytes(self) -> int:
+        B, L, C, H = self.n_batch, self.seq_len, self.c_in, self.n_heads
+        return 2 * B * L * L * C + 2 * B * H * L * L + 2 * H * C + 8 * C
+
+
+PAIR_BIAS_WORKLOADS = [
+    PairBiasWorkload("pb_msa_row_bf16", 1, 256, 128, 8, seed=4001,
+                     description="MSA row attention pair bias: z [256, 256, 128] -> [8, 256, 256]"),
+    PairBiasWorkload("pb_tri_start_bf16", 1, 256, 128, 4, seed=4002,
+                     description="triangle attention (starting node) bias: z [256, 256, 128] -> [4, 256, 256]"),
+    PairBiasWorkload("pb_tri_end_bf16", 1, 256, 128, 4, transpose=True, seed=4003,
+                     description="triangle attention (ending node) bias, transposed layout"),
+]
+
+
+def pair_bias_by_name(name: str) -> PairBiasWorkload:
+    for w in PAIR_BIAS_WORKLOADS:
+        if w.name == name:
+            return w
+    raise KeyError(name)
+
+
+def generate_pair_bias(w: PairBiasWorkload, seed: Optional[int] = None) -> Dict[str, np.ndarray]:
+    """z [B, L, L, C] and weight [H, C] as bf16 bits; ln_weight, ln_bias fp32."""
+    rng = np.random.Generator(np.random.PCG64(w.seed if seed is None else seed))
+    B, L, C, H = w.n_batch, w.seq_len, w.c_in, w.n_heads
+    offset = rng.standard_normal((B, L, L, 1)) * 2.0
+    spread = rng.uniform(0.25, 4.0, size=(B, L, L, 1))
+    z = rng.standard_normal((B, L, L, C)) * spread + offset
+    lnw = (1.0 + 0.2 * rng.standard_normal(C)).astype(np.float32)
+    lnb = (0.2 * rng.standard_normal(C)).astype(np.float32)
+    W = rng.standard_normal((H, C)) / math.sqrt(C)
+    return {"z": _store(z, "bf16"), "ln_weight": lnw, "ln_bias": lnb, "weight": _store(W, "bf16")}

@@ -25,8 +25,9 @@ def test_exports_declared_symbol():
     lib = _lib()
     decls = re.findall(r"^\s*int\s*(evo_\w+)\s*\(", open(os.path.join(ROOT, "include", "evo_proj.h")).read(),
                        flags=re.M)
-    assert decls == ["evo_ln_proj_fwd"]
-    assert hasattr(lib, "evo_ln_proj_fwd")
+    assert decls == ["evo_ln_proj_fwd", "evo_ln_pair_bias_fwd"]
+    for name in decls:
+        assert hasattr(lib, name), name
 
 
 def _call(dims, x=FAKE, lnw=FAKE + 0x10000, lnb=FAKE + 0x11000, w=FAKE + 0x20000, b=None,

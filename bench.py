@@ -112,6 +112,9 @@ def main():
     if args.workload.startswith("pb_"):
         pair_bias_bench(torch, args)
         return
+    if args.workload.startswith("adam_"):
+        optim_bench(torch, args)
+        return
 
     w = W.by_name(args.workload)
     x = W.generate(w)
@@ -581,6 +584,92 @@ def pair_bias_bench(torch, args):
     print(json.dumps(line))
 
 
+def optim_bench(torch, args):
+    """Optimizer step over every parameter tensor of an AlphaFold-sized model:
+    gradient-norm clipping (two kernels) then the fused Adam + SWA kernel.
+    `value` is algorithmic HBM bytes per second of the whole step."""
+    from paper_2404_11068_amd import optim as op
+    from paper_2404_11068_amd import workloads as W
+
+    w = W.optim_by_name(args.workload)
+    d = W.generate_optim(w)
+    dev = lambda lst: [torch.from_numpy(a).cuda() for a in lst]
+    P, G, M, V, S = (dev(d[k]) for k in ("params", "grads", "exp_avg", "exp_avg_sq", "swa"))
+    opt = op.FusedAdamSWA(P, G, M, V, S, lr=w.lr, betas=w.betas, eps=w.eps, swa_decay=w.swa_decay)
+    stream = torch.cuda.current_stream()
+    step_no = [w.step]
+
+    def step():
+        opt.step(max_norm=w.max_norm, stream=stream, step=step_no[0])
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    start, stop = mk(), mk()
+    t0 = time.perf_counter()
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = start.elapsed_time(stop) / args.steps
+    # per phase: clipping (sum-of-squares + scale kernels), then the Adam + SWA kernel alone
+    ev = [[mk() for _ in range(3)] for _ in range(args.steps)]
+    for l_ in ev:
+        for e in l_:
+            e.record(stream)
+    torch.cuda.synchronize()
+    for e0, e1, e2 in ev:
+        e0.record(stream)
+        opt.clip(w.max_norm, stream)
+        e1.record(stream)
+        opt.step(max_norm=None, stream=stream, step=step_no[0])
+        e2.record(stream)
+    torch.cuda.synchronize()
+    clip_ms = [a.elapsed_time(b) for a, b, _ in ev]
+    adam_ms = [b.elapsed_time(c) for _, b, c in ev]
+    k_ms = float(np.mean(adam_ms))
+    nbytes = w.bytes_step()
+    ach = nbytes / (k_ms * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": measured_traffic("adam_swa_kernel", w.name),
+                "kernel": "adam_swa_kernel", "avg_ms": round(k_ms, 5), "algorithmic_bytes": int(nbytes)}
+    total = nbytes + w.bytes_clip()
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import optim_oracle as oo
+        sub = slice(None, None, 10)
+        f64 = {k: [a.astype(np.float64) for a in d[k][sub]] for k in d}
+        n_sub = sum(a.size for a in f64["params"])
+        reps, ts = 0, []
+        while sum(ts) < args.cpu_seconds and reps < 50:
+            t1 = time.perf_counter()
+            _, sc = oo.grad_norm_scale(f64["grads"], w.max_norm)
+            oo.adam_swa_step(f64["params"], f64["grads"], f64["exp_avg"], f64["exp_avg_sq"], f64["swa"], lr=w.lr,
+                             beta1=w.betas[0], beta2=w.betas[1], eps=w.eps, weight_decay=0.0, step=w.step,
+                             swa_decay=w.swa_decay, grad_scale=sc)
+            ts.append(time.perf_counter() - t1)
+            reps += 1
+        t = float(np.median(ts))
+        cpu = {"value": round(40 * n_sub / t / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+               "cpu_model": _cpu_model(), "seconds_per_run": round(t, 4), "runs": reps,
+               "sample": "every 10th tensor (%d elements), clipping + Adam + SWA in numpy fp64, median of %d runs"
+                         % (n_sub, reps)}
+    line = {
+        "metric": "Optimizer step (grad clipping + fused Adam + SWA over all parameters), GB/s on 1 MI355X",
+        "value": round(total / (ms_step * 1e-3) / 1e9, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": w.name, "tensors": len(P), "elements": w.numel(), "chunks": opt.n_chunks,
+                   "max_norm": w.max_norm, "parallelism": "single-gpu"},
+        "clip_ms": _pct(clip_ms), "adam_swa_ms": _pct(adam_ms),
+        "wall_s": round(wall, 3), "roofline": roofline, "cpu_baseline": cpu,
+    }
+    print(json.dumps(line))
+
+
 def proj_cpu_baseline(w, d, target_s: float):
     """The fp64 oracle (LayerNorm + one numpy matmul per projection) on the
     host, on a slice of rows sized for about target_s."""
@@ -667,7 +756,8 @@ def measured_traffic(kernel: str, workload: str):
 KERNEL_SOURCES = {"attn": ("evo_frag.h", "evo_fwd.hip", "evo_bwd.hip"),
                   "ln": ("evo_frag.h", "evo_ln.hip"),
                   "proj": ("evo_frag.h", "evo_proj.hip"),
-                  "pb": ("evo_frag.h", "evo_pair_bias.hip")}
+                  "pb": ("evo_frag.h", "evo_pair_bias.hip"),
+                  "optim": ("evo_frag.h", "evo_optim.hip")}
 
 
 def kernel_family(kernel: str) -> str:
@@ -675,6 +765,8 @@ def kernel_family(kernel: str) -> str:
         return "proj"
     if kernel.startswith("pair_bias"):
         return "pb"
+    if kernel in ("adam_swa_kernel", "sumsq_kernel", "clip_scale_kernel"):
+        return "optim"
     return "ln" if kernel.startswith("ln_") else "attn"
 
 

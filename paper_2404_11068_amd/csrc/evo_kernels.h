@@ -120,3 +120,15 @@ bool proj_supported(int C, int HD, int P);
 hipError_t launch_ln_proj(const PjArgs &a, hipStream_t s);
 
 }  // namespace evo
+
+// fused optimizer step (types from include/evo_optim.h)
+struct evo_mt_tensor;
+struct evo_mt_chunk;
+struct evo_adam_swa_hparams;
+namespace evo {
+hipError_t launch_adam_swa(const evo_adam_swa_hparams &hp, const evo_mt_tensor *tensors, int32_t n_tensors,
+                           const evo_mt_chunk *chunks, int32_t n_chunks, const float *grad_scale, hipStream_t s);
+hipError_t launch_clip_scale(const evo_mt_tensor *tensors, int32_t n_tensors, const evo_mt_chunk *chunks,
+                             int32_t n_chunks, float max_norm, float *ws, float *norm_out, float *scale_out,
+                             hipStream_t s);
+}  // namespace evo

@@ -345,3 +345,131 @@ def generate_pair_bias(w: PairBiasWorkload, seed: Optional[int] = None) -> Dict[
     lnb = (0.2 * rng.standard_normal(C)).astype(np.float32)
     W = rng.standard_normal((H, C)) / math.sqrt(C)
     return {"z": _store(z, "bf16"), "ln_weight": lnw, "ln_bias": lnb, "weight": _store(W, "bf16")}
+
+
+# ---------------------------------------------------------------------------
+# Optimizer step: the parameter tensors of an AlphaFold-sized model.  The
+# paper trains a 97M-parameter model with over four thousand gradient tensors
+# (ScaleFold Sections 2.2 and 3.3); the shapes below follow the Evoformer
+# block at the standard widths (c_m = 256, c_z = 128, 8 MSA heads of 32,
+# 4 pair heads of 32, transitions x4, outer product mean c = 32, triangle
+# multiplication c = 128), repeated for 48 main blocks, 4 extra-MSA blocks
+# (c_e = 64) and 2 template pair blocks (c_t = 64), plus embedding and
+# structure-module sized extras.  Values: params ~ N(0, 0.02^2), grads ~
+# N(0, 1e-3^2), Adam moments from a few earlier steps (m ~ N(0, 1e-4^2),
+# v ~ |N(0, 1e-6^2)|), SWA copy = params + N(0, 1e-4^2).
+
+def _evoformer_block_shapes(c_m: int, c_z: int, pair_only: bool = False):
+    s = []
+
+    def lin(cin, cout, bias=True):
+        s.append((cout, cin))
+        if bias:
+            s.append((cout,))
+
+    def ln(c):
+        s.extend([(c,), (c,)])
+
+    hm, dm, hz, dz = 8, 32, 4, 32
+    if not pair_only:
+        # MSA row attention with pair bias, MSA column attention, MSA transition, outer product mean
+        ln(c_m); ln(c_z); lin(c_z, hm, bias=False)
+        for _ in range(3):
+            lin(c_m, hm * dm, bias=False)
+        lin(c_m, hm * dm); lin(hm * dm, c_m)
+        ln(c_m)
+        for _ in range(3):
+            lin(c_m, hm * dm, bias=False)
+        lin(c_m, hm * dm); lin(hm * dm, c_m)
+        ln(c_m); lin(c_m, 4 * c_m); lin(4 * c_m, c_m)
+        ln(c_m); lin(c_m, 32); lin(c_m, 32); lin(32 * 32, c_z)
+    # triangle multiplication (outgoing, incoming)
+    for _ in range(2):
+        ln(c_z)
+        for _ in range(4):
+            lin(c_z, 128)
+        lin(c_z, c_z); ln(128); lin(128, c_z)
+    # triangle attention (starting, ending node)
+    for _ in range(2):
+        ln(c_z); lin(c_z, hz, bias=False)
+        for _ in range(3):
+            lin(c_z, hz * dz, bias=False)
+        lin(c_z, hz * dz); lin(hz * dz, c_z)
+    # pair transition
+    ln(c_z); lin(c_z, 4 * c_z); lin(4 * c_z, c_z)
+    return s
+
+
+def alphafold_param_shapes():
+    shapes = []
+    for _ in range(48):
+        shapes += _evoformer_block_shapes(256, 128)
+    for _ in range(4):
+        shapes += _evoformer_block_shapes(64, 128)
+    for _ in range(2):
+        shapes += _evoformer_block_shapes(64, 64, pair_only=True)
+    # embedders, recycling, structure module and heads (approximate sizes)
+    extras = [(256, 49), (256,), (128, 22), (128,), (128, 22), (128,), (128, 65), (128,), (64, 25), (64,),
+              (256, 256), (256,), (128, 15), (128,), (384, 256), (384,), (384, 384), (384,), (384, 384), (384,),
+              (1152, 384), (1152,), (384, 1152), (384,), (128, 384), (128,), (50, 128), (50,), (64, 128), (64,),
+              (23, 256), (23,), (37 * 14, 384), (256, 39), (128, 39)]
+    for _ in range(8):
+        extras += [(384, 384), (384,), (384,), (384,)]
+    return shapes + extras
+
+
+@dataclasses.dataclass(frozen=True)
+class OptimWorkload:
+    name: str
+    subset: int = 0          # 0 = all tensors, else every subset-th tensor
+    max_norm: float = 0.1
+    lr: float = 1e-3
+    betas: tuple = (0.9, 0.999)
+    eps: float = 1e-6
+    swa_decay: float = 0.999
+    step: int = 10
+    seed: int = 0
+    description: str = ""
+
+    def shapes(self):
+        sh = alphafold_param_shapes()
+        return sh if not self.subset else sh[::self.subset]
+
+    def numel(self) -> int:
+        return int(sum(int(np.prod(s)) for s in self.shapes()))
+
+    def bytes_step(self) -> int:
+        # read p, g, m, v, swa; write p, m, v, swa (fp32)
+        return 36 * self.numel()
+
+    def bytes_clip(self) -> int:
+        return 4 * self.numel()
+
+
+OPTIM_WORKLOADS = [
+    OptimWorkload("adam_swa_alphafold", seed=5001,
+                  description="all parameter tensors of an AlphaFold-sized model (fp32 master weights)"),
+    OptimWorkload("adam_swa_small", subset=37, seed=5002,
+                  description="every 37th tensor of the same model (a parity-test size)"),
+]
+
+
+def optim_by_name(name: str) -> OptimWorkload:
+    for w in OPTIM_WORKLOADS:
+        if w.name == name:
+            return w
+    raise KeyError(name)
+
+
+def generate_optim(w: OptimWorkload, seed: Optional[int] = None):
+    """Lists of fp32 arrays: params, grads, exp_avg, exp_avg_sq, swa (one per tensor)."""
+    rng = np.random.Generator(np.random.PCG64(w.seed if seed is None else seed))
+    out = {k: [] for k in ("params", "grads", "exp_avg", "exp_avg_sq", "swa")}
+    for s in w.shapes():
+        p = rng.standard_normal(s, dtype=np.float32) * np.float32(0.02)
+        out["params"].append(p)
+        out["grads"].append(rng.standard_normal(s, dtype=np.float32) * np.float32(1e-3))
+        out["exp_avg"].append(rng.standard_normal(s, dtype=np.float32) * np.float32(1e-4))
+        out["exp_avg_sq"].append(np.abs(rng.standard_normal(s, dtype=np.float32)) * np.float32(1e-6))
+        out["swa"].append(p + rng.standard_normal(s, dtype=np.float32) * np.float32(1e-4))
+    return out

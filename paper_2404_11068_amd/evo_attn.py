@@ -121,6 +121,9 @@ def _mask_u8(m: Optional[torch.Tensor]) -> Optional[torch.Tensor]:
 
 
 def _stream(stream) -> ctypes.c_void_p:
+    """hipStream_t of a torch stream (None: the current one) or a raw handle (int)."""
+    if isinstance(stream, int):
+        return ctypes.c_void_p(stream)
     s = torch.cuda.current_stream() if stream is None else stream
     return ctypes.c_void_p(s.cuda_stream)
 

@@ -94,7 +94,7 @@ __global__ __launch_bounds__(64 * kPjWaves) void ln_proj_kernel(PjArgs a) {
                 bv[4 * q + e] = b4[e];
             }
         }
-        const bool stats = a.mean != nullptr;
+        const bool stats = a.mean != nullptr && blockIdx.y == 0;  // one writer per token tile
         const rsrc_t rm = make_buf(stats ? a.mean + row0 : nullptr, stats ? (uint32_t)nrows * 4u : 0u);
         const rsrc_t rr = make_buf(stats ? a.rstd + row0 : nullptr, stats ? (uint32_t)nrows * 4u : 0u);
         constexpr float inv_c = 1.0f / (float)C;
@@ -135,10 +135,16 @@ __global__ __launch_bounds__(64 * kPjWaves) void ln_proj_kernel(PjArgs a) {
 
     // ---- 2./3. projections -------------------------------------------------
     const int n = lane & 31, h = lane >> 5;
-    const int NF = a.P * a.HD / 32;
+    // feature tiles of this workgroup: group blockIdx.y of gridDim.y equal
+    // contiguous groups (more than one only when the tokens alone would leave
+    // CUs idle)
+    const int NFall = a.P * a.HD / 32;
+    const int per = (NFall + (int)gridDim.y - 1) / (int)gridDim.y;
+    const int fbeg = (int)blockIdx.y * per;
+    const int NF = NFall < fbeg + per ? NFall : fbeg + per;
     const rsrc_t rW = make_buf(a.W, (uint32_t)(a.P * a.HD) * C * 2u);
     const rsrc_t rB = make_buf(a.bias, a.bias ? (uint32_t)(a.P * a.HD) * 4u : 0u);
-    int f = wave;
+    int f = fbeg + wave;
     if (f >= NF) return;  // wave-uniform; no barrier follows
 
     for (; f < NF; f += kPjWaves) {
@@ -210,7 +216,13 @@ template <int C, int TB>
 hipError_t ln_proj_c(const PjArgs &a, hipStream_t s) {
     const int64_t tm = 32 * TB;
     const int64_t nwg = (a.R + tm - 1) / tm;
-    hipLaunchKernelGGL((ln_proj_kernel<C, TB>), dim3((unsigned)nwg), dim3(64 * kPjWaves), 0, s, a);
+    // fewer token tiles than CUs: split the feature tiles over up to NF/8
+    // workgroups per token tile (each recomputes the tile's LayerNorm)
+    const int nf = a.P * a.HD / 32;
+    int64_t fs = nwg < 256 ? 256 / nwg : 1;
+    const int64_t fs_max = nf / kPjWaves > 1 ? nf / kPjWaves : 1;
+    fs = fs < fs_max ? fs : fs_max;
+    hipLaunchKernelGGL((ln_proj_kernel<C, TB>), dim3((unsigned)nwg, (unsigned)fs), dim3(64 * kPjWaves), 0, s, a);
     return hipGetLastError();
 }
 

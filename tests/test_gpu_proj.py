@@ -75,6 +75,8 @@ CASES = [
     (513, 256, 32, 2, True, True),
     (64, 256, 1024, 1, False, False),
     (129, 64, 160, 4, True, True),
+    (4096, 256, 256, 4, True, True),    # fewer token tiles than CUs: features split over workgroups
+    (300, 128, 128, 4, False, True),
 ]
 
 

@@ -11,8 +11,9 @@
 // wave, a pair entry of C channels is read by LPR = C / 8 lanes (16 bytes
 // each; all the wave's loads are issued before any arithmetic).  LayerNorm
 // statistics come from DPP row reductions; the normalised entry is rounded
-// to bf16 and each head's dot product is four v_dot2_f32_bf16 per lane plus
-// a DPP row reduction.  The H x 4 x 32 results go through LDS so that the
+// to bf16 and each head's dot product is four v_dot2_f32_bf16 per lane; the
+// H partial sums are then reduce-scattered over the entry's lanes (each lane
+// ends with the full sum of one head, or of H/LPR heads).  The H x 4 x 32 results go through LDS so that the
 // stores cover 16 contiguous bytes (plain layout) or 8 (transposed).
 // Lengths are multiples of 8, so no 16- or 8-byte piece straddles a row.
 #include "evo_frag.h"
@@ -34,6 +35,45 @@ __device__ __forceinline__ float pb_row_sum(float v) {
     if constexpr (LPR >= 16) v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x140, 0xF, 0xF, false));
     if constexpr (LPR >= 32) v += __shfl_xor(v, 16, 64);
     return v;
+}
+
+// value of the partner lane at distance M inside an LPR-lane group: xor 16
+// crosses 16-lane rows (ds_bpermute); 8 and 4 use the row and half-row
+// mirrors (partner 15-i, 7-i: the bit M differs and every higher bit is
+// shared, which is all the reductions below need); 2 and 1 swap pairs.
+template <int M>
+__device__ __forceinline__ float pb_partner(float v) {
+    if constexpr (M == 16) return __shfl_xor(v, 16, 64);
+    constexpr int ctrl = M == 8 ? 0x140 : M == 4 ? 0x141 : M == 2 ? 0x4E : 0xB1;
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), ctrl, 0xF, 0xF, false));
+}
+
+// Reduce-scatter of H per-lane partial sums over an LPR-lane group: at each
+// lane bit (highest first) the lanes split their current set of heads in
+// halves, keep one half and add the partner's values for it (sending the
+// other half); once one head is left the remaining bits are plain pairwise
+// sums.  Afterwards the lane holds the full sums of heads [*first, *first +
+// KEEP) with KEEP = max(1, H / LPR).  Cost: about H + log2(LPR) exchanges
+// instead of H * log2(LPR) for one full reduction per head.
+template <int LPR, int H, int M = LPR / 2, int CNT = H>
+__device__ __forceinline__ void pb_reduce_scatter(float (&v)[H], int li, int *first) {
+    if constexpr (M >= 1) {
+        if constexpr (CNT > 1) {
+            constexpr int HALF = CNT / 2;
+            const bool upper = (li & M) != 0;
+#pragma unroll
+            for (int k = 0; k < HALF; ++k) {
+                const float send = upper ? v[k] : v[HALF + k];
+                const float keep = upper ? v[HALF + k] : v[k];
+                v[k] = keep + pb_partner<M>(send);
+            }
+            if (upper) *first += HALF;
+            pb_reduce_scatter<LPR, H, M / 2, HALF>(v, li, first);
+        } else {
+            v[0] += pb_partner<M>(v[0]);
+            pb_reduce_scatter<LPR, H, M / 2, 1>(v, li, first);
+        }
+    }
 }
 
 __device__ __forceinline__ void bstore8(u32x2 v, rsrc_t r, uint32_t off) {
@@ -125,23 +165,26 @@ __global__ __launch_bounds__(64 * kPbWaves) void pair_bias_kernel(PbArgs a) {
             y[q][0] = (__bf16)fmaf(f[2 * q] * rstd, wv[2 * q], bv[2 * q]);
             y[q][1] = (__bf16)fmaf(f[2 * q + 1] * rstd, wv[2 * q + 1], bv[2 * q + 1]);
         }
-        // lane li keeps head li (and li + LPR, ...) of its entry
-        float mine[(H + LPR - 1) / LPR];
-#pragma unroll
-        for (int k = 0; k < (H + LPR - 1) / LPR; ++k) mine[k] = 0.f;
+        // one partial dot product per head over this lane's 8 channels, then
+        // a reduce-scatter over the entry's lanes
+        float dh[H];
 #pragma unroll
         for (int h = 0; h < H; ++h) {
             float d = 0.f;
 #pragma unroll
             for (int q = 0; q < 4; ++q) d = __builtin_amdgcn_fdot2_f32_bf16(y[q], wh[h][q], d, false);
-            d = pb_row_sum<LPR>(d);
-            if (li == h % LPR) mine[h / LPR] = d;
+            dh[h] = d;
         }
+        int first = 0;
+        pb_reduce_scatter<LPR, H>(dh, li, &first);
+        constexpr int KEEP = H > LPR ? H / LPR : 1;
+        // lanes that differ only in the bits summed after the split hold the
+        // same heads: the one with those bits clear writes them
+        constexpr int DUP = H >= LPR ? 1 : LPR / H;
         const int p = s * PPS + rs;
+        if ((li & (DUP - 1)) == 0) {
 #pragma unroll
-        for (int k = 0; k < (H + LPR - 1) / LPR; ++k) {
-            const int h = k * LPR + li;
-            if (h < H) stage[h][wave][p] = __builtin_bit_cast(uint16_t, (__bf16)mine[k]);
+            for (int k = 0; k < KEEP; ++k) stage[first + k][wave][p] = __builtin_bit_cast(uint16_t, (__bf16)dh[k]);
         }
         const int j = j0 + p;
         const uint32_t so = (li == 0 && j < Lj) ? (uint32_t)j * 4u : kOOB;

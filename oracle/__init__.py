@@ -221,3 +221,27 @@ def pair_bias_forward(z, ln_weight, ln_bias, weight, eps: float = 1e-5, transpos
     if transpose:
         out = np.swapaxes(out, 2, 3)          # [B, H, Lj, Li]
     return np.ascontiguousarray(out)
+
+
+def ln_proj_backward(x, ln_weight, ln_bias, weight, douts, eps: float = 1e-5):
+    """Gradients of ln_proj_forward for upstream gradients douts[p] ([..., HD]):
+    (dx, dln_weight, dln_bias, dweight [n_proj*HD, C], dbias [n_proj*HD]).
+
+    With y = LN(x):  dY = sum_p dout_p @ W_p;  (dx, dln_weight, dln_bias) is the
+    LayerNorm backward of dY;  dW_p = dout_p^T @ y;  dbias_p = sum over tokens
+    of dout_p.  Matmuls are library primitives (numpy, fp64)."""
+    x = _f64(x)
+    W = _f64(weight)
+    C = x.shape[-1]
+    P = len(douts)
+    HD = W.shape[0] // P
+    x2 = x.reshape(-1, C)
+    y, _, _ = layernorm_forward(x2, ln_weight, ln_bias, eps)
+    d2 = [_f64(d).reshape(-1, HD) for d in douts]
+    dY = np.zeros_like(x2)
+    for p in range(P):
+        dY += d2[p] @ W[p * HD:(p + 1) * HD]
+    dx, dlw, dlb = layernorm_backward(x2, dY, ln_weight, eps)
+    dW = np.concatenate([d2[p].T @ y for p in range(P)], axis=0)
+    db = np.concatenate([d2[p].sum(axis=0) for p in range(P)])
+    return dx.reshape(x.shape), dlw, dlb, dW, db

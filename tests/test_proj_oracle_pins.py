@@ -77,3 +77,46 @@ def test_three_dim_input():
     o3 = oracle.ln_proj_forward(x.reshape(3, 4, -1), lw, lb, W, b, n_proj=4)
     for p in range(4):
         np.testing.assert_allclose(o3[p].reshape(12, -1), o2[p], rtol=1e-14, atol=1e-14)
+
+
+@pytest.mark.parametrize("P", [1, 4])
+def test_backward_matches_torch_autograd(P):
+    x, lw, lb, W, b = _case(6, R=11, C=16, HD=8, P=P)
+    rng = np.random.default_rng(8)
+    douts = [rng.standard_normal((11, 8)) for _ in range(P)]
+    xt = torch.tensor(x, requires_grad=True)
+    lwt = torch.tensor(lw, requires_grad=True)
+    lbt = torch.tensor(lb, requires_grad=True)
+    Wt = torch.tensor(W, requires_grad=True)
+    bt = torch.tensor(b, requires_grad=True)
+    y = F.layer_norm(xt, (16,), lwt, lbt, 1e-5)
+    loss = sum((F.linear(y, Wt[p * 8:(p + 1) * 8], bt[p * 8:(p + 1) * 8]) * torch.tensor(douts[p])).sum()
+               for p in range(P))
+    loss.backward()
+    dx, dlw, dlb, dW, db = oracle.ln_proj_backward(x, lw, lb, W, douts, 1e-5)
+    np.testing.assert_allclose(dx, xt.grad.numpy(), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dlw, lwt.grad.numpy(), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dlb, lbt.grad.numpy(), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dW, Wt.grad.numpy(), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(db, bt.grad.numpy(), rtol=1e-10, atol=1e-12)
+
+
+def test_backward_finite_differences():
+    x, lw, lb, W, b = _case(9, R=3, C=5, HD=2, P=2)
+    rng = np.random.default_rng(10)
+    douts = [rng.standard_normal((3, 2)) for _ in range(2)]
+
+    def loss(x_, W_):
+        outs = oracle.ln_proj_forward(x_, lw, lb, W_, b, n_proj=2)
+        return sum(float((o * d).sum()) for o, d in zip(outs, douts))
+
+    dx, _, _, dW, _ = oracle.ln_proj_backward(x, lw, lb, W, douts)
+    h = 1e-6
+    for arr, grad, which in ((x, dx, 0), (W, dW, 1)):
+        num = np.zeros_like(arr)
+        for i in np.ndindex(arr.shape):
+            a1, a2 = arr.copy(), arr.copy()
+            a1[i] += h
+            a2[i] -= h
+            num[i] = ((loss(a1, W) - loss(a2, W)) if which == 0 else (loss(x, a1) - loss(x, a2))) / (2 * h)
+        np.testing.assert_allclose(grad, num, rtol=1e-6, atol=1e-7)

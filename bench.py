@@ -15,6 +15,7 @@ bounded sample of the same workload on the host cores.
 from __future__ import annotations
 
 import argparse
+import ctypes
 import json
 import os
 import sys
@@ -473,6 +474,34 @@ def proj_bench(torch, args):
         torch.cuda.synchronize()
         res[mode] = [a.elapsed_time(b_) for a, b_ in ev]
     del flush
+    # backward (training forward saves the normalised input): dY product,
+    # LayerNorm backward, weight-gradient product and the partial sums
+    y = torch.empty_like(x)
+    _, mean, rstd = pj.ln_proj_fwd(x, lnw, lnb, Wt, b, n_proj=w.n_proj, eps=w.eps, need_stats=True, y_norm=y,
+                                   stream=stream)
+    gen = torch.Generator(device="cpu").manual_seed(w.seed + 1)
+    douts = [torch.randn(w.n_rows, w.proj_dim, generator=gen).to(torch.bfloat16).cuda() for _ in range(w.n_proj)]
+    bufs = dict(dx=torch.empty_like(x), dweight=torch.empty(w.n_proj * w.proj_dim, w.c_in, device="cuda"),
+                dbias=torch.empty(w.n_proj * w.proj_dim, device="cuda") if b is not None else None,
+                dln_weight=torch.empty(w.c_in, device="cuda"), dln_bias=torch.empty(w.c_in, device="cuda"))
+    wsb = torch.empty(max(1, int(pj._lib().evo_ln_proj_bwd_workspace_size(ctypes.byref(
+        pj.evo_proj_dims(1, w.c_in, w.n_proj, w.proj_dim, w.n_rows, w.eps, 0))))), dtype=torch.uint8, device="cuda")
+
+    def bwd():
+        pj.ln_proj_bwd(x, lnw, mean, rstd, y, Wt, douts, eps=w.eps, has_bias=b is not None, workspace=wsb,
+                       stream=stream, **bufs)
+
+    for _ in range(args.warmup):
+        bwd()
+    torch.cuda.synchronize()
+    bev = [(mk(), mk()) for _ in range(args.steps)]
+    for a_, b2 in bev:
+        a_.record(stream)
+        bwd()
+        b2.record(stream)
+    torch.cuda.synchronize()
+    bwd_ms = [a_.elapsed_time(b2) for a_, b2 in bev]
+    bwd_flops = 2.0 * w.flops()
     k_ms = float(np.mean(res["warm"]))
     nbytes = w.bytes()
     ach = nbytes / (k_ms * 1e-3) / 1e9
@@ -491,6 +520,8 @@ def proj_bench(torch, args):
         "config": {"workload": w.name, "n_rows": w.n_rows, "c_in": w.c_in, "n_proj": w.n_proj,
                    "proj_dim": w.proj_dim, "bias": w.bias, "parallelism": "single-gpu"},
         "gbs": round(nbytes / (ms_step * 1e-3) / 1e9, 1),
+        "bwd_ms": _pct(bwd_ms),
+        "bwd_tflops": round(bwd_flops / (float(np.median(bwd_ms)) * 1e-3) / 1e12, 2),
         "timing": {"warm": {"note": "calls back to back", "ms": _pct(res["warm"])},
                    "cold": {"note": "512 MiB scratch written before each call, outside the events",
                             "ms": _pct(res["cold"])}},
@@ -675,7 +706,8 @@ def optim_bench(torch, args):
 
 GRAPH_WORKLOADS = {
     # MSA row attention with pair bias at one GPU's share under 8-way dynamic axial parallelism
-    # (128 MSA rows / 8 = 16 rows of 256 residues), and the whole 128-row module
+    # (128 MSA rows / 8 = 16 rows of 256 residues), and the whole 128-row module; one step is the
+    # projections, the pair bias, attention forward and backward and the projections' backward
     "graph_msa_row_dap8": dict(N=16, L=256),
     "graph_msa_row_full": dict(N=128, L=256),
     # a launch-bound size: 4 rows of 64 residues (GPU work well below the host's launch cost)
@@ -685,8 +717,9 @@ GRAPH_WORKLOADS = {
 
 def graph_bench(torch, args):
     """One MSA-row-attention step (LayerNorm + q/k/v/g projections, pair bias,
-    attention forward and backward: 4 C-ABI calls, 8 kernels) run eagerly
-    through the Python binding and replayed from the HIP graph cache.
+    attention forward and backward, projection + LayerNorm backward: 5 C-ABI
+    calls, 14 kernels) run eagerly through the Python binding and replayed
+    from the HIP graph cache.
     `value` is graphed steps per second; the eager rate, the host time to
     enqueue one step and the speedup are reported beside it."""
     from paper_2404_11068_amd import graph as gr
@@ -723,9 +756,11 @@ def graph_bench(torch, args):
     g = res["graph"]["wall_ms_per_step"]
     N, L, H, d, c_m, c_z = cfg["N"], cfg["L"], 8, 32, 256, 128
     tok = N * L * H * d * 2
-    nbytes = (2 * N * L * c_m + 4 * tok + 2 * 4 * H * d * c_m) + (2 * L * L * c_z + 2 * H * L * L) + \
+    nbytes = (2 * N * L * c_m + 4 * tok + 2 * 4 * H * d * c_m + 2 * N * L * c_m + 8 * N * L) + \
+        (2 * L * L * c_z + 2 * H * L * L) + \
         (4 * tok + 2 * H * L * L + N * L + tok + 4 * N * H * L) + \
-        (6 * tok + 4 * N * H * L + 2 * H * L * L + N * L + 4 * tok + 4 * H * L * L)
+        (6 * tok + 4 * N * H * L + 2 * H * L * L + N * L + 4 * tok + 4 * H * L * L) + \
+        (4 * tok + 3 * 2 * N * L * c_m + 8 * N * L + 2 * 4 * H * d * c_m + 4 * 4 * H * d * c_m)
     ach = nbytes / (res["graph"]["gpu_ms_per_step"] * 1e-3) / 1e9
     line = {
         "metric": "MSA row attention step (projections, pair bias, attention fwd+bwd) from the HIP graph cache, "
@@ -734,7 +769,7 @@ def graph_bench(torch, args):
         "ms_per_step": g, "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": args.workload, "n_rows": N, "seq_len": L, "n_heads": H, "head_dim": d, "c_m": c_m,
-                   "c_z": c_z, "kernels_per_step": 8, "parallelism": "single-gpu"},
+                   "c_z": c_z, "kernels_per_step": 14, "parallelism": "single-gpu"},
         "eager": res["eager"], "graph": res["graph"],
         "speedup_wall": round(res["eager"]["wall_ms_per_step"] / g, 3),
         "host_enqueue_reduction": round(res["eager"]["host_enqueue_ms_per_step"] /

@@ -56,6 +56,37 @@ int evo_ln_proj_fwd(const evo_proj_dims *dims, const void *x, const float *ln_we
                     const float *ln_bias, const void *weight, const float *bias,
                     void *const *outs, float *mean, float *rstd, void *stream);
 
+/* Training variant: as evo_ln_proj_fwd, and when y_norm is not NULL also
+ * writes the normalised input LayerNorm(x) as rounded to bf16 for the
+ * products (contiguous [R, C] bf16, 16-byte aligned), which the backward
+ * reads. */
+int evo_ln_proj_fwd_ex(const evo_proj_dims *dims, const void *x, const float *ln_weight,
+                       const float *ln_bias, const void *weight, const float *bias,
+                       void *const *outs, float *mean, float *rstd, void *y_norm, void *stream);
+
+/*
+ * Backward of the fused LayerNorm + projections.  With y = y_norm (the
+ * forward's normalised input) and upstream gradients douts[p] ([R, HD] bf16,
+ * a HOST array of n_proj device pointers):
+ *
+ *   dY       = sum_p douts[p] @ weight[p*HD:(p+1)*HD, :]   rounded to bf16
+ *   dx, dln_weight, dln_bias = LayerNorm backward of dY (as evo_layernorm_bwd,
+ *              from x, ln_weight and the forward's mean, rstd)
+ *   dweight[p*HD + f, c] = sum_t douts[p][t, f] * y[t, c]   (fp32)
+ *   dbias[p*HD + f]      = sum_t douts[p][t, f]             (fp32; NULL: not computed)
+ *
+ * dx: [R, C] bf16 output; dweight: [n_proj*HD, C] fp32; dbias: [n_proj*HD]
+ * fp32 or NULL; dln_weight, dln_bias: [C] fp32 (all 16-byte aligned).
+ * workspace: at least evo_ln_proj_bwd_workspace_size(dims) bytes, 256-byte
+ * aligned, contents irrelevant.  Every sum runs in a fixed order (repeatable
+ * results).  R == 0 validates and returns EVO_OK without touching anything.
+ */
+size_t evo_ln_proj_bwd_workspace_size(const evo_proj_dims *dims);
+int evo_ln_proj_bwd(const evo_proj_dims *dims, const void *x, const float *ln_weight, const float *mean,
+                    const float *rstd, const void *y_norm, const void *weight, const void *const *douts,
+                    void *dx, float *dweight, float *dbias, float *dln_weight, float *dln_bias,
+                    void *workspace, size_t workspace_bytes, void *stream);
+
 /*
  * Pair bias: the logit bias every pair-biased Evoformer attention adds before
  * its softmax (ScaleFold Section 3.3, "Multi Head Attention"), a LayerNorm of

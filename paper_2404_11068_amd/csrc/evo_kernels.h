@@ -96,10 +96,35 @@ struct PjArgs {
     const float *bias;        // [P*HD] or null
     void *out0, *out1, *out2, *out3;  // [R, HD] bf16 each (first P used)
     float *mean, *rstd;       // [R] or null (both or neither)
+    void *y;                  // [R, C] bf16 normalised input (saved for the backward) or null
     int64_t R;
     int C, HD, P;
     float eps;
 };
+
+// backward of the fused LayerNorm + projections
+struct PjBwdArgs {
+    const void *x;            // [R, C] bf16
+    const float *lnw;         // [C]
+    const float *mean, *rstd; // [R]
+    const void *y;            // [R, C] bf16 normalised input from the forward
+    const void *W;            // [P*HD, C] bf16
+    const void *dout0, *dout1, *dout2, *dout3;  // [R, HD] bf16
+    void *dx;                 // [R, C] bf16
+    float *dW;                // [P*HD, C]
+    float *dbias;             // [P*HD] or null
+    float *dlnw, *dlnb;       // [C]
+    int64_t R;
+    int C, HD, P;
+};
+
+struct PjBwdPlan {
+    int64_t n_chunks, chunk_tokens;   // token chunks of the weight-gradient pass
+    size_t off_dy, off_ln, off_dw, off_db, total;
+};
+
+PjBwdPlan plan_proj_bwd(int64_t R, int C, int HD, int P);
+hipError_t launch_ln_proj_bwd(const PjBwdArgs &a, void *ws, const PjBwdPlan &plan, hipStream_t s);
 
 // LayerNorm of pair entries projected to per-head logit biases (bf16)
 struct PbArgs {

@@ -133,6 +133,16 @@ __global__ __launch_bounds__(64 * kPjWaves) void ln_proj_kernel(PjArgs a) {
     }
     __syncthreads();
 
+    // ---- the normalised tile itself, for the backward (optional) -----------
+    if (a.y) {
+        const rsrc_t ry = make_buf((char *)a.y + row0 * C * 2, (uint32_t)nrows * C * 2);
+        constexpr int CH = C / 8;  // 16-byte chunks per row
+        for (int idx = threadIdx.x; idx < G::TM * CH; idx += 64 * kPjWaves) {
+            const int r = idx / CH, c = idx % CH;
+            bstore16(*(const u32x4 *)(lds + r * G::STRIDE + c * 16), ry, (uint32_t)(r * C + c * 8) * 2u);
+        }
+    }
+
     // ---- 2./3. projections -------------------------------------------------
     const int n = lane & 31, h = lane >> 5;
     // feature tiles of this workgroup: group blockIdx.y of gridDim.y equal

@@ -15,22 +15,38 @@ bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0;
 
 extern "C" {
 
-int evo_ln_proj_fwd(const evo_proj_dims *d, const void *x, const float *ln_weight, const float *ln_bias,
-                    const void *weight, const float *bias, void *const *outs, float *mean, float *rstd,
-                    void *stream) {
+namespace {
+
+int check_proj(const evo_proj_dims *d) {
     if (!d || d->reserved != 0) return EVO_ERR_INVALID_ARG;
     if (d->dtype != EVO_DTYPE_BF16) return EVO_ERR_UNSUPPORTED;
     if (d->n_rows < 0 || d->c_in < 1 || d->n_proj < 1 || d->proj_dim < 1 || !(d->eps >= 0.0f) ||
         !isfinite(d->eps))
         return EVO_ERR_INVALID_ARG;
     if (!evo::proj_supported(d->c_in, d->proj_dim, d->n_proj)) return EVO_ERR_UNSUPPORTED;
-    // the kernels address one workgroup's rows with 32-bit offsets; the grid is 32-bit
     if (d->n_rows > (int64_t(1) << 36)) return EVO_ERR_UNSUPPORTED;
+    return EVO_OK;
+}
+
+}  // namespace
+
+int evo_ln_proj_fwd(const evo_proj_dims *d, const void *x, const float *ln_weight, const float *ln_bias,
+                    const void *weight, const float *bias, void *const *outs, float *mean, float *rstd,
+                    void *stream) {
+    return evo_ln_proj_fwd_ex(d, x, ln_weight, ln_bias, weight, bias, outs, mean, rstd, nullptr, stream);
+}
+
+int evo_ln_proj_fwd_ex(const evo_proj_dims *d, const void *x, const float *ln_weight, const float *ln_bias,
+                       const void *weight, const float *bias, void *const *outs, float *mean, float *rstd,
+                       void *y_norm, void *stream) {
+    const int st = check_proj(d);
+    if (st) return st;
     if (d->n_rows == 0) return EVO_OK;
     if (!x || !ln_weight || !ln_bias || !weight || !outs) return EVO_ERR_INVALID_ARG;
     if ((mean == nullptr) != (rstd == nullptr) || (mean && (void *)mean == (void *)rstd)) return EVO_ERR_INVALID_ARG;
+    if (y_norm && (y_norm == x || !aligned(y_norm, 16))) return y_norm == x ? EVO_ERR_INVALID_ARG : EVO_ERR_ALIGNMENT;
     for (int p = 0; p < d->n_proj; ++p) {
-        if (!outs[p] || outs[p] == x || outs[p] == weight) return EVO_ERR_INVALID_ARG;
+        if (!outs[p] || outs[p] == x || outs[p] == weight || outs[p] == y_norm) return EVO_ERR_INVALID_ARG;
         for (int q = 0; q < p; ++q)
             if (outs[q] == outs[p]) return EVO_ERR_INVALID_ARG;
         if (!aligned(outs[p], 16)) return EVO_ERR_ALIGNMENT;
@@ -52,12 +68,62 @@ int evo_ln_proj_fwd(const evo_proj_dims *d, const void *x, const float *ln_weigh
     a.out3 = o[3];
     a.mean = mean;
     a.rstd = rstd;
+    a.y = y_norm;
     a.R = d->n_rows;
     a.C = d->c_in;
     a.HD = d->proj_dim;
     a.P = d->n_proj;
     a.eps = d->eps;
     return evo::launch_ln_proj(a, (hipStream_t)stream) == hipSuccess ? EVO_OK : EVO_ERR_HIP;
+}
+
+size_t evo_ln_proj_bwd_workspace_size(const evo_proj_dims *d) {
+    if (check_proj(d)) return 0;
+    return evo::plan_proj_bwd(d->n_rows, d->c_in, d->proj_dim, d->n_proj).total;
+}
+
+int evo_ln_proj_bwd(const evo_proj_dims *d, const void *x, const float *ln_weight, const float *mean,
+                    const float *rstd, const void *y_norm, const void *weight, const void *const *douts, void *dx,
+                    float *dweight, float *dbias, float *dln_weight, float *dln_bias, void *workspace,
+                    size_t workspace_bytes, void *stream) {
+    int st = check_proj(d);
+    if (st) return st;
+    if (d->n_rows == 0) return EVO_OK;
+    if (!x || !ln_weight || !mean || !rstd || !y_norm || !weight || !douts || !dx || !dweight || !dln_weight ||
+        !dln_bias)
+        return EVO_ERR_INVALID_ARG;
+    for (int p = 0; p < d->n_proj; ++p) {
+        if (!douts[p]) return EVO_ERR_INVALID_ARG;
+        if (!aligned(douts[p], 16)) return EVO_ERR_ALIGNMENT;
+    }
+    if (dx == x || dx == y_norm || (void *)dln_weight == (void *)dln_bias) return EVO_ERR_INVALID_ARG;
+    const void *al16[] = {x, y_norm, weight, dx, dweight, dln_weight, dln_bias, ln_weight};
+    for (const void *q : al16)
+        if (!aligned(q, 16)) return EVO_ERR_ALIGNMENT;
+    if ((dbias && !aligned(dbias, 16)) || !aligned(mean, 4) || !aligned(rstd, 4)) return EVO_ERR_ALIGNMENT;
+    const evo::PjBwdPlan plan = evo::plan_proj_bwd(d->n_rows, d->c_in, d->proj_dim, d->n_proj);
+    if (!workspace || workspace_bytes < plan.total || !aligned(workspace, 256)) return EVO_ERR_WORKSPACE;
+    evo::PjBwdArgs a{};
+    a.x = x;
+    a.lnw = ln_weight;
+    a.mean = mean;
+    a.rstd = rstd;
+    a.y = y_norm;
+    a.W = weight;
+    a.dout0 = douts[0];
+    a.dout1 = d->n_proj > 1 ? douts[1] : nullptr;
+    a.dout2 = d->n_proj > 2 ? douts[2] : nullptr;
+    a.dout3 = d->n_proj > 3 ? douts[3] : nullptr;
+    a.dx = dx;
+    a.dW = dweight;
+    a.dbias = dbias;
+    a.dlnw = dln_weight;
+    a.dlnb = dln_bias;
+    a.R = d->n_rows;
+    a.C = d->c_in;
+    a.HD = d->proj_dim;
+    a.P = d->n_proj;
+    return evo::launch_ln_proj_bwd(a, workspace, plan, (hipStream_t)stream) == hipSuccess ? EVO_OK : EVO_ERR_HIP;
 }
 
 int evo_ln_pair_bias_fwd(const evo_pair_bias_dims *d, const void *z, const float *ln_weight, const float *ln_bias,

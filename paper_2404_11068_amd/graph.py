@@ -8,8 +8,9 @@ library's kernels on it (no allocation, no synchronisation).
 
 `MSARowAttentionStep` is the work of one MSA row attention with pair bias
 (LayerNorm + q/k/v/gate projections, LayerNorm(z) + pair-bias projection,
-attention forward, attention backward) on static buffers, runnable eagerly
-(one C-ABI call per stage) or through the cache (one graph launch).
+attention forward, attention backward, backward of the projections and their
+LayerNorm) on static buffers, runnable eagerly (one C-ABI call per stage) or
+through the cache (one graph launch).
 """
 from __future__ import annotations
 
@@ -124,6 +125,18 @@ class MSARowAttentionStep:
         self.dq, self.dk, self.dv, self.dg = (torch.empty(N, L, H, d, **bf) for _ in range(4))
         self.dbias = torch.empty(1, H, L, L, **f32)
         self.ws = torch.empty(max(ea.evo_attn_bwd_workspace_size(self.q, N), 1), dtype=torch.uint8, device=device)
+        # training forward state of the projections and their gradients
+        self.y_norm = torch.empty_like(self.m)
+        self.mean = torch.empty(N, L, **f32)
+        self.rstd = torch.empty(N, L, **f32)
+        self.dm = torch.empty_like(self.m)
+        self.dw_qkvg = torch.empty(4 * H * d, c_m, **f32)
+        self.db_qkvg = torch.empty(4 * H * d, **f32)
+        self.dln_m_w = torch.empty(c_m, **f32)
+        self.dln_m_b = torch.empty(c_m, **f32)
+        dims = pj.evo_proj_dims(1, c_m, 4, H * d, N * L, 1e-5, 0)
+        self.ws_proj = torch.empty(max(int(pj._lib().evo_ln_proj_bwd_workspace_size(ctypes.byref(dims))), 1),
+                                   dtype=torch.uint8, device=device)
 
         self._key = hash((N, L, H, d, self.m.data_ptr(), self.z.data_ptr(), self.dq.data_ptr())) & \
             0xFFFFFFFFFFFFFFFF
@@ -133,16 +146,21 @@ class MSARowAttentionStep:
         return self._key
 
     def record(self, stream):
-        """Enqueue the step (4 C-ABI calls, 8 kernels) on `stream` (torch stream or raw handle)."""
+        """Enqueue the step (5 C-ABI calls, 14 kernels) on `stream` (torch stream or raw handle)."""
         pj.ln_proj_fwd(self.m, self.ln_m_w, self.ln_m_b, self.w_qkvg, self.b_qkvg, n_proj=4,
-                       outs=[t.view(self.N, self.L, -1) for t in (self.q, self.k, self.v, self.gate)], stream=stream)
+                       outs=[t.view(self.N, self.L, -1) for t in (self.q, self.k, self.v, self.gate)],
+                       mean=self.mean, rstd=self.rstd, y_norm=self.y_norm, stream=stream)
         pj.ln_pair_bias_fwd(self.z, self.ln_z_w, self.ln_z_b, self.w_bias, out=self.bias, stream=stream)
         ea.evo_attn_fwd(self.q, self.k, self.v, self.gate, self.bias, self.mask, rows_per_bias=self.N,
                         out=self.out, lse=self.lse, stream=stream)
         ea.evo_attn_bwd(self.q, self.k, self.v, self.gate, self.bias, self.mask, self.out, self.lse, self.dout,
                         rows_per_bias=self.N, dq=self.dq, dk=self.dk, dv=self.dv, dgate=self.dg, dbias=self.dbias,
                         workspace=self.ws, stream=stream)
+        pj.ln_proj_bwd(self.m, self.ln_m_w, self.mean, self.rstd, self.y_norm, self.w_qkvg,
+                       [t.view(self.N, self.L, -1) for t in (self.dq, self.dk, self.dv, self.dg)],
+                       dx=self.dm, dweight=self.dw_qkvg, dbias=self.db_qkvg, dln_weight=self.dln_m_w,
+                       dln_bias=self.dln_m_b, workspace=self.ws_proj, stream=stream)
 
     def outputs(self):
         return {k: getattr(self, k) for k in ("q", "k", "v", "gate", "bias", "out", "lse", "dq", "dk", "dv", "dg",
-                                               "dbias")}
+                                               "dbias", "y_norm", "dm", "dw_qkvg", "db_qkvg", "dln_m_w", "dln_m_b")}

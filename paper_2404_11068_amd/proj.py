@@ -36,6 +36,14 @@ def _lib():
         P = ctypes.c_void_p
         lib.evo_ln_proj_fwd.argtypes = [ctypes.POINTER(evo_proj_dims), P, P, P, P, P, ctypes.POINTER(P), P, P, P]
         lib.evo_ln_proj_fwd.restype = ctypes.c_int
+        lib.evo_ln_proj_fwd_ex.argtypes = [ctypes.POINTER(evo_proj_dims), P, P, P, P, P, ctypes.POINTER(P), P, P,
+                                           P, P]
+        lib.evo_ln_proj_fwd_ex.restype = ctypes.c_int
+        lib.evo_ln_proj_bwd_workspace_size.argtypes = [ctypes.POINTER(evo_proj_dims)]
+        lib.evo_ln_proj_bwd_workspace_size.restype = ctypes.c_size_t
+        lib.evo_ln_proj_bwd.argtypes = [ctypes.POINTER(evo_proj_dims), P, P, P, P, P, P, ctypes.POINTER(P), P, P, P,
+                                        P, P, P, ctypes.c_size_t, P]
+        lib.evo_ln_proj_bwd.restype = ctypes.c_int
         _bound = True
     return lib
 
@@ -43,11 +51,13 @@ def _lib():
 def ln_proj_fwd(x: torch.Tensor, ln_weight: torch.Tensor, ln_bias: torch.Tensor, weight: torch.Tensor,
                 bias: Optional[torch.Tensor] = None, n_proj: int = 4, eps: float = 1e-5, *,
                 outs: Optional[List[torch.Tensor]] = None, mean=None, rstd=None, need_stats: bool = False,
-                stream=None) -> List[torch.Tensor]:
+                y_norm: Optional[torch.Tensor] = None, stream=None) -> List[torch.Tensor]:
     """outs[p] = LayerNorm(x) @ weight[p*HD:(p+1)*HD].T + bias[p*HD:(p+1)*HD].
 
     With need_stats (or mean/rstd given) the LayerNorm statistics are stored
-    too and returned after the outputs: (outs, mean, rstd)."""
+    too and returned after the outputs: (outs, mean, rstd).  With y_norm (a
+    bf16 tensor shaped like x) the normalised input is saved there for
+    ln_proj_bwd."""
     lib = _lib()
     if x.dtype != torch.bfloat16 or weight.dtype != torch.bfloat16:
         raise ValueError("x and weight must be bfloat16")
@@ -68,13 +78,52 @@ def ln_proj_fwd(x: torch.Tensor, ln_weight: torch.Tensor, ln_bias: torch.Tensor,
         rstd = torch.empty(x.shape[:-1], dtype=torch.float32, device=x.device) if rstd is None else rstd
     d = evo_proj_dims(EVO_DTYPE_BF16, C, n_proj, HD, R, float(eps), 0)
     ptrs = (ctypes.c_void_p * n_proj)(*[ctypes.c_void_p(o.data_ptr()) for o in outs])
-    st = lib.evo_ln_proj_fwd(ctypes.byref(d), _ptr(x), _ptr(ln_weight), _ptr(ln_bias), _ptr(weight), _ptr(bias),
-                             ptrs, _ptr(mean), _ptr(rstd), _stream(stream))
+    if y_norm is not None and (y_norm.dtype != torch.bfloat16 or not y_norm.is_contiguous()
+                               or y_norm.numel() != x.numel()):
+        raise ValueError("y_norm must be a contiguous bf16 tensor shaped like x")
+    st = lib.evo_ln_proj_fwd_ex(ctypes.byref(d), _ptr(x), _ptr(ln_weight), _ptr(ln_bias), _ptr(weight),
+                                _ptr(bias), ptrs, _ptr(mean), _ptr(rstd), _ptr(y_norm), _stream(stream))
     if st:
-        raise EvoAttnError(st, "evo_ln_proj_fwd")
+        raise EvoAttnError(st, "evo_ln_proj_fwd_ex")
     if mean is not None:
         return outs, mean, rstd
     return outs
+
+
+def ln_proj_bwd(x, ln_weight, mean, rstd, y_norm, weight, douts, *, eps: float = 1e-5, has_bias: bool = True,
+                dx=None, dweight=None, dbias=None, dln_weight=None, dln_bias=None, workspace=None, stream=None):
+    """Gradients (dx, dweight, dbias or None, dln_weight, dln_bias) of
+    ln_proj_fwd for upstream gradients douts (one [..., HD] bf16 tensor per
+    projection), from the forward's statistics and saved normalised input."""
+    lib = _lib()
+    P = len(douts)
+    C = x.shape[-1]
+    HD = weight.shape[0] // P
+    R = x.numel() // C if C else 0
+    for t in list(douts) + [x, y_norm, weight]:
+        if t.dtype != torch.bfloat16 or not t.is_contiguous():
+            raise ValueError("x, y_norm, weight and douts must be contiguous bfloat16")
+    if any(t.numel() != R * HD for t in douts) or y_norm.numel() != R * C:
+        raise ValueError("douts must hold R*HD elements and y_norm R*C")
+    dev = x.device
+    dx = torch.empty_like(x) if dx is None else dx
+    dweight = torch.empty((P * HD, C), dtype=torch.float32, device=dev) if dweight is None else dweight
+    if has_bias and dbias is None:
+        dbias = torch.empty(P * HD, dtype=torch.float32, device=dev)
+    dln_weight = torch.empty(C, dtype=torch.float32, device=dev) if dln_weight is None else dln_weight
+    dln_bias = torch.empty(C, dtype=torch.float32, device=dev) if dln_bias is None else dln_bias
+    d = evo_proj_dims(EVO_DTYPE_BF16, C, P, HD, R, float(eps), 0)
+    need = int(lib.evo_ln_proj_bwd_workspace_size(ctypes.byref(d)))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    ptrs = (ctypes.c_void_p * P)(*[ctypes.c_void_p(t.data_ptr()) for t in douts])
+    st = lib.evo_ln_proj_bwd(ctypes.byref(d), _ptr(x), _ptr(ln_weight), _ptr(mean), _ptr(rstd), _ptr(y_norm),
+                             _ptr(weight), ptrs, _ptr(dx), _ptr(dweight), _ptr(dbias if has_bias else None),
+                             _ptr(dln_weight), _ptr(dln_bias), _ptr(workspace),
+                             ctypes.c_size_t(workspace.numel() * workspace.element_size()), _stream(stream))
+    if st:
+        raise EvoAttnError(st, "evo_ln_proj_bwd")
+    return dx, dweight, (dbias if has_bias else None), dln_weight, dln_bias
 
 
 class evo_pair_bias_dims(ctypes.Structure):

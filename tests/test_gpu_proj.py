@@ -109,3 +109,103 @@ def test_empty():
     one, zero = torch.ones(128, device="cuda"), torch.zeros(128, device="cuda")
     outs = pj.ln_proj_fwd(x, one, zero, Wt, None, n_proj=4)
     assert all(o.shape == (0, 64) for o in outs)
+
+
+# ---- backward ---------------------------------------------------------------
+# Tolerances: dx (bf16): per element 4 x the shift the bf16 rounding of dY
+# can cause (2^-9 rstd times |w dY| plus the row means of |w dY| and
+# |w dY xhat| |xhat|) plus 2^-8 |ref|, and 1e-2 normwise; dweight (fp32 sums over R
+# tokens of products whose y factor was rounded to bf16): normwise 5e-3 and
+# element-wise 5e-3|ref| + 5e-3 max|ref|; dbias (exact bf16 inputs, fp32
+# sums): 1e-5 relative + 1e-5 max; dln_weight, dln_bias (sums of bf16-rounded
+# dY terms): normwise 5e-3, element-wise 1e-2|ref| + 5e-3 max|ref|.
+
+
+def run_bwd(w, d, label, seed=0):
+    print("\n[case] bwd", label, flush=True)
+    x = to_device(d["x"], "bf16")
+    Wt = to_device(d["weight"], "bf16")
+    lnw, lnb = torch.from_numpy(d["ln_weight"]).cuda(), torch.from_numpy(d["ln_bias"]).cuda()
+    b = None if d["bias"] is None else torch.from_numpy(d["bias"]).cuda()
+    y = torch.empty_like(x)
+    outs, mean, rstd = pj.ln_proj_fwd(x, lnw, lnb, Wt, b, n_proj=w.n_proj, eps=w.eps, need_stats=True, y_norm=y)
+    rng = np.random.default_rng(seed + 17)
+    douts_np = [W._store(rng.standard_normal((w.n_rows, w.proj_dim)), "bf16") for _ in range(w.n_proj)]
+    douts = [to_device(a, "bf16") for a in douts_np]
+    dx, dW, db, dlw, dlb = pj.ln_proj_bwd(x, lnw, mean, rstd, y, Wt, douts, eps=w.eps, has_bias=b is not None)
+    torch.cuda.synchronize()
+    ref = oracle.ln_proj_backward(W.as_float64(d["x"], "bf16"), d["ln_weight"], d["ln_bias"],
+                                  W.as_float64(d["weight"], "bf16"), [W.as_float64(a, "bf16") for a in douts_np],
+                                  w.eps)
+    rdx, rdlw, rdlb, rdW, rdb = ref
+    # dx: the kernel rounds dY to bf16 before the LayerNorm backward, which
+    # moves dx[r, c] by up to rstd_r |w_c| |dY_rc| 2^-9 whatever the size of
+    # dx itself; allow 4x that per element plus the output's own rounding
+    xf = W.as_float64(d["x"], "bf16")
+    _, _, rrstd = oracle.layernorm_forward(xf, None, None, w.eps)
+    Wf = W.as_float64(d["weight"], "bf16")
+    HD = w.proj_dim
+    dY = sum(W.as_float64(douts_np[p_], "bf16") @ Wf[p_ * HD:(p_ + 1) * HD] for p_ in range(w.n_proj))
+    # (the row means of g = w dY and g xhat in the LayerNorm backward carry
+    # the same relative rounding, averaged over the row)
+    _, rmean, _ = oracle.layernorm_forward(xf, None, None, w.eps)
+    xhat = (xf - rmean[:, None]) * rrstd[:, None]
+    g = np.abs(d["ln_weight"])[None, :] * np.abs(dY)
+    row = g.mean(axis=1)[:, None] + np.abs(xhat) * (g * np.abs(xhat)).mean(axis=1)[:, None]
+    bound = 4 * 2.0 ** -9 * rrstd[:, None] * (g + row) + 2.0 ** -8 * np.abs(rdx)
+    gdx = to_f64(dx).reshape(rdx.shape)
+    err = np.abs(gdx - rdx)
+    i = int(np.argmax(err - bound - 1e-6))
+    assert (err <= bound + 1e-6).all(), (label, "dx err %.3g at ref %.3g (bound %.3g)" %
+                                         (err.flat[i], rdx.flat[i], bound.flat[i]))
+    rel = np.linalg.norm(gdx - rdx) / np.linalg.norm(rdx)
+    assert rel <= 1e-2, (label, "dx normwise %.3g" % rel)
+    m = np.abs(rdW).max()
+    _check(label + " dW", to_f64(dW), rdW, atol=5e-3 * m, rtol=5e-3, norm=5e-3)
+    if db is not None:
+        _check(label + " dbias", to_f64(db), rdb, atol=1e-5 * np.abs(rdb).max(), rtol=1e-5, norm=1e-5)
+    for nm, g, r in (("dln_w", dlw, rdlw), ("dln_b", dlb, rdlb)):
+        _check(label + " " + nm, to_f64(g), r, atol=5e-3 * np.abs(r).max(), rtol=1e-2, norm=5e-3)
+    # the saved normalised input is the forward's bf16 LayerNorm
+    yref, _, _ = oracle.layernorm_forward(W.as_float64(d["x"], "bf16"), d["ln_weight"], d["ln_bias"], w.eps)
+    _check(label + " y", to_f64(y), yref, norm=5e-3)
+
+
+@pytest.mark.parametrize("name", [w.name for w in W.PROJ_WORKLOADS])
+def test_backward_full_workload(name):
+    w = W.proj_by_name(name)
+    run_bwd(w, W.generate_proj(w), name)
+
+
+BWD_CASES = [
+    # R, C, HD, P, bias
+    (1, 64, 32, 1, False),
+    (77, 256, 256, 4, True),
+    (300, 128, 96, 3, True),
+    (1000, 64, 64, 4, True),
+    (129, 64, 160, 2, False),
+    (4100, 256, 32, 4, True),
+]
+
+
+@pytest.mark.parametrize("case", BWD_CASES, ids=lambda c: "R%d_C%d_HD%d_P%d_b%d" % c)
+def test_backward_shapes(case):
+    R, C, HD, P, bias = case
+    w = W.ProjWorkload("adhoc", R, C, HD, n_proj=P, bias=bias, seed=R + 3 * C + HD)
+    run_bwd(w, W.generate_proj(w), str(case), seed=R)
+
+
+def test_backward_repeatable():
+    w = W.ProjWorkload("adhoc", 3000, 128, 128, seed=4)
+    d = W.generate_proj(w)
+    x = to_device(d["x"], "bf16")
+    Wt = to_device(d["weight"], "bf16")
+    lnw, lnb = torch.from_numpy(d["ln_weight"]).cuda(), torch.from_numpy(d["ln_bias"]).cuda()
+    y = torch.empty_like(x)
+    _, mean, rstd = pj.ln_proj_fwd(x, lnw, lnb, Wt, None, n_proj=4, need_stats=True, y_norm=y)
+    douts = [torch.randn(3000, 128, device="cuda").to(torch.bfloat16) for _ in range(4)]
+    a = pj.ln_proj_bwd(x, lnw, mean, rstd, y, Wt, douts)
+    b = pj.ln_proj_bwd(x, lnw, mean, rstd, y, Wt, douts)
+    torch.cuda.synchronize()
+    for u, v in zip(a, b):
+        assert torch.equal(u, v)

@@ -23,9 +23,10 @@ def _lib():
 
 def test_exports_declared_symbol():
     lib = _lib()
-    decls = re.findall(r"^\s*int\s*(evo_\w+)\s*\(", open(os.path.join(ROOT, "include", "evo_proj.h")).read(),
-                       flags=re.M)
-    assert decls == ["evo_ln_proj_fwd", "evo_ln_pair_bias_fwd"]
+    decls = re.findall(r"^\s*(?:int|size_t)\s*(evo_\w+)\s*\(",
+                       open(os.path.join(ROOT, "include", "evo_proj.h")).read(), flags=re.M)
+    assert set(decls) == {"evo_ln_proj_fwd", "evo_ln_proj_fwd_ex", "evo_ln_proj_bwd_workspace_size",
+                          "evo_ln_proj_bwd", "evo_ln_pair_bias_fwd"}
     for name in decls:
         assert hasattr(lib, name), name
 
@@ -75,3 +76,36 @@ def test_rejects_bad_pointers():
 
 def test_empty_needs_no_pointers():
     assert _call(_dims(n_rows=0), x=None, lnw=None, lnb=None, w=None, outs=None) == 0
+
+
+def _bwd(dims, x=FAKE, lnw=FAKE + 0x10000, mean=FAKE + 0x11000, rstd=FAKE + 0x12000, y=FAKE + 0x100000,
+         w=FAKE + 0x200000, douts=(FAKE + 0x300000, FAKE + 0x400000, FAKE + 0x500000, FAKE + 0x600000),
+         dx=FAKE + 0x700000, dW=FAKE + 0x800000, db=None, dlw=FAKE + 0x900000, dlb=FAKE + 0x901000,
+         ws=FAKE + 0x1000000, ws_bytes=1 << 30):
+    lib = _lib()
+    arr = None if douts is None else (ctypes.c_void_p * len(douts))(*[ctypes.c_void_p(o) if o else None
+                                                                      for o in douts])
+    return lib.evo_ln_proj_bwd(ctypes.byref(dims) if dims is not None else None, P(x), P(lnw), P(mean), P(rstd),
+                               P(y), P(w), arr, P(dx), P(dW), P(db), P(dlw), P(dlb), P(ws),
+                               ctypes.c_size_t(ws_bytes), None)
+
+
+def test_backward_rejects_bad_calls():
+    lib = _lib()
+    d = _dims()
+    assert _bwd(_dims(c_in=96)) == 2
+    assert _bwd(None) == 1
+    for k in ("x", "lnw", "mean", "rstd", "y", "w", "dx", "dW", "dlw", "dlb"):
+        assert _bwd(d, **{k: None}) == 1, k
+    assert _bwd(d, douts=None) == 1
+    assert _bwd(d, douts=(FAKE + 0x300000, None, FAKE + 0x500000, FAKE + 0x600000)) == 1
+    assert _bwd(d, dx=FAKE) == 1
+    assert _bwd(d, dlb=FAKE + 0x900000) == 1
+    assert _bwd(d, y=FAKE + 0x100008) == 3
+    assert _bwd(d, douts=(FAKE + 0x300004, FAKE + 0x400000, FAKE + 0x500000, FAKE + 0x600000)) == 3
+    need = lib.evo_ln_proj_bwd_workspace_size(ctypes.byref(d))
+    assert need > 0
+    assert _bwd(d, ws_bytes=need - 1) == 4
+    assert _bwd(d, ws=None) == 4
+    assert _bwd(_dims(n_rows=0), x=None, y=None, w=None, douts=None, dx=None) == 0
+    assert lib.evo_ln_proj_bwd_workspace_size(ctypes.byref(_dims(c_in=96))) == 0

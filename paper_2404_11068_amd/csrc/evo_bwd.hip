@@ -370,7 +370,10 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(4
     constexpr int CPT = D / VEC;            // 16-byte chunks per token
     constexpr int LP = NKT * 32;
     constexpr int NT = NKT * 64;
-    constexpr int KSTR = D + VEC;           // row stride of K, V, Q, dA tiles in LDS (elements)
+    // bf16 rows of 32 channels use the swizzled 64-byte layout (sw32);
+    // otherwise rows are padded by one 16-byte chunk
+    constexpr bool kSw = kTr && D == 32;
+    constexpr int KSTR = kSw ? D : D + VEC;  // row stride of K, V, Q, dA tiles in LDS (elements)
     constexpr int NKV = (LP * CPT + NT - 1) / NT;  // 16-byte chunks of K (and of V) per thread
     constexpr int NQC = (32 * CPT + NT - 1) / NT;  // 16-byte chunks of the Q (and dA) tile per thread
     constexpr int NSUM = (32 * (D / 4) + NT - 1) / NT;  // 4-channel groups of dQ summed per thread
@@ -468,8 +471,9 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(4
             const int idx = tid + j * NT;
             if (idx < LP * CPT) {
                 const int t = idx / CPT, c = (idx % CPT) * VEC;
-                *reinterpret_cast<u32x4 *>(&k_lds[t * KSTR + c]) = kr[j];
-                *reinterpret_cast<u32x4 *>(&v_lds[t * KSTR + c]) = vr[j];
+                const int o = kSw ? sw32(t, idx % CPT) : t * KSTR + c;
+                *reinterpret_cast<u32x4 *>(&k_lds[o]) = kr[j];
+                *reinterpret_cast<u32x4 *>(&v_lds[o]) = vr[j];
             }
         }
 #pragma unroll
@@ -477,8 +481,9 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(4
             const int idx = tid + j * NT;
             if (idx < 32 * CPT) {
                 const int t = idx / CPT, c = (idx % CPT) * VEC;
-                *reinterpret_cast<u32x4 *>(&q_lds[t * KSTR + c]) = qr[j];
-                *reinterpret_cast<u32x4 *>(&da_lds[t * KSTR + c]) = dar[j];
+                const int o = kSw ? sw32(t, idx % CPT) : t * KSTR + c;
+                *reinterpret_cast<u32x4 *>(&q_lds[o]) = qr[j];
+                *reinterpret_cast<u32x4 *>(&da_lds[o]) = dar[j];
             }
         }
         if (tid < 32) {
@@ -500,10 +505,17 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(4
         f32x16 dq = zero16();
         if (kbits != 0) {
             ChFrag<T, D> qb, dab, ka, va;
-            qb.load(&q_lds[n * KSTR], h2);
-            dab.load(&da_lds[n * KSTR], h2);
-            ka.load(&k_lds[(kt * 32 + sig(n)) * KSTR], h2);
-            va.load(&v_lds[(kt * 32 + sig(n)) * KSTR], h2);
+            if constexpr (kSw) {
+                load_sw32(qb, q_lds, n, h2);
+                load_sw32(dab, da_lds, n, h2);
+                load_sw32(ka, k_lds, kt * 32 + sig(n), h2);
+                load_sw32(va, v_lds, kt * 32 + sig(n), h2);
+            } else {
+                qb.load(&q_lds[n * KSTR], h2);
+                dab.load(&da_lds[n * KSTR], h2);
+                ka.load(&k_lds[(kt * 32 + sig(n)) * KSTR], h2);
+                va.load(&v_lds[(kt * 32 + sig(n)) * KSTR], h2);
+            }
             const float l2 = lse2_lds[n], ds = dsum_lds[n];
             // S^T = K Q^T, dP^T = V dA^T: lane = query, reg i = key kt*32 + krow(i, h2)
             f32x16 S = zero16(), dP = zero16();
@@ -529,7 +541,9 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(4
             }
             // dQ^T (channels x queries) = K^T dS^T over this wave's keys
             K32 kT;
-            if constexpr (kTr) {
+            if constexpr (kSw) {
+                kT = load_k32_tr_sw32(k_lds, kt * 32, lane);
+            } else if constexpr (kTr) {
                 kT = load_k32_tr(k_lds, KSTR, kt * 32, D, lane);
             } else {
                 const int c = sig(n);

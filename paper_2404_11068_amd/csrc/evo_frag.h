@@ -275,6 +275,43 @@ __device__ __forceinline__ Tr<bf16_t>::K32 load_k32_tr(const uint16_t *X, int st
 }
 
 // ---------------------------------------------------------------------------
+// Swizzled LDS tile of bf16 rows of 32 channels (64 bytes, no padding): the
+// 16-byte chunk k (channels 8k..8k+7) of row t sits at chunk k ^ ((t >> 2) & 3).
+// With 64 four-byte banks, 16 lanes reading one chunk of 16 consecutive rows,
+// 16 lanes writing the four chunks of four consecutive rows, and the
+// transposing read below (four consecutive rows, all chunks, per 32 lanes)
+// all touch each bank once.  A padded 40-element stride left two-way
+// conflicts on the row-major writes and the transposing reads.
+__device__ __forceinline__ int sw32(int row, int chunk) { return row * 32 + ((chunk ^ ((row >> 2) & 3)) << 3); }
+
+// ChFrag<bf16_t, 32> of `row` from a swizzled tile: channels 16kk + 8h + s
+__device__ __forceinline__ void load_sw32(ChFrag<bf16_t, 32> &f, const uint16_t *tile, int row, int h) {
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) f.v[kk] = *reinterpret_cast<const bf16x8 *>(tile + sw32(row, 2 * kk + h));
+}
+
+// load_k32_tr(X, 32, kbase, 32, lane) for a swizzled tile: each lane's
+// 8-byte piece lies inside one chunk, so only the chunk index moves
+__device__ __forceinline__ Tr<bf16_t>::K32 load_k32_tr_sw32(const uint16_t *X, int kbase, int lane) {
+    const int G = lane >> 4, i = lane & 15;
+    const int q = i & 3;
+    const int c0 = 16 * (G & 1) + 4 * (((q & 1) << 1) | (q >> 1));
+    const int rbase = kbase + 8 * (G >> 1) + (i >> 2);
+    Tr<bf16_t>::K32 f;
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+        const int r0 = rbase + 16 * t, r1 = r0 + 4;
+        const uint16_t *s0 = X + sw32(r0, c0 >> 3) + (c0 & 7);
+        const uint16_t *s1 = X + sw32(r1, c0 >> 3) + (c0 & 7);
+        const short4tr lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) short4tr *)(s0));
+        const short4tr hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) short4tr *)(s1));
+        const short8tr both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        f.v[t] = __builtin_bit_cast(bf16x8, both);
+    }
+    return f;
+}
+
+// ---------------------------------------------------------------------------
 // Constant A operand "c times a permuted identity" for the k32 contraction:
 // A[m][k] = c where k-slot k holds row sig(m) of the tile, else 0.  With a B
 // operand holding X[k][n] (k = key row of the tile, n = query), the product

@@ -85,7 +85,7 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (reference for HBM byte counters)")
     ap.add_argument("--source-hash", nargs="?", const="attn", default=None, choices=sorted(KERNEL_SOURCES),
-                    help="print the source hash of a kernel family (attn, ln) and exit")
+                    help="print the source hash of a kernel family and exit")
     args = ap.parse_args()
     if args.source_hash:
         print(kernel_source_hash(args.source_hash))
@@ -869,6 +869,7 @@ def measured_traffic(kernel: str, workload: str):
 KERNEL_SOURCES = {"attn": ("evo_frag.h", "evo_fwd.hip", "evo_bwd.hip"),
                   "ln": ("evo_frag.h", "evo_ln.hip"),
                   "proj": ("evo_frag.h", "evo_proj.hip"),
+                  "proj_bwd": ("evo_frag.h", "evo_proj_bwd.hip"),
                   "pb": ("evo_frag.h", "evo_pair_bias.hip"),
                   "optim": ("evo_frag.h", "evo_optim.hip")}
 
@@ -876,6 +877,8 @@ KERNEL_SOURCES = {"attn": ("evo_frag.h", "evo_fwd.hip", "evo_bwd.hip"),
 def kernel_family(kernel: str) -> str:
     if kernel.startswith("ln_proj"):
         return "proj"
+    if kernel in ("dy_kernel", "dw_kernel", "colsum_kernel"):
+        return "proj_bwd"
     if kernel.startswith("pair_bias"):
         return "pb"
     if kernel in ("adam_swa_kernel", "sumsq_kernel", "clip_scale_kernel"):

@@ -77,28 +77,30 @@ __device__ __forceinline__ const void *dout_ptr(const PjBwdArgs &a, int p) {
 // stage are issued four stages ahead into a ring of register stages, in one
 // in-order stream (the memory counter retires loads in issue order, so a
 // wait for one load is a wait for every older one).
-template <int C>
+// A workgroup covers CW of the C channels (CW < C splits the channels over
+// blockIdx.y when there are too few token blocks to fill the GPU).
+template <int CW>
 struct DyCfg {
-    static constexpr int NW = C >= 128 ? 16 : 8;
+    static constexpr int NW = CW >= 128 ? 16 : 8;
     static constexpr int NT = 64 * NW;
 };
 
-template <int C>
-__global__ __launch_bounds__(DyCfg<C>::NT) void dy_kernel(PjBwdArgs a, void *__restrict__ dy) {
-    constexpr int NW = DyCfg<C>::NW, NT = DyCfg<C>::NT;
+template <int C, int CW>
+__global__ __launch_bounds__(DyCfg<CW>::NT) void dy_kernel(PjBwdArgs a, void *__restrict__ dy) {
+    constexpr int NW = DyCfg<CW>::NW, NT = DyCfg<CW>::NT;
     constexpr int TM = 128, KC = 64, NR = 4;
-    constexpr int NCT = C / 32, CG = NW / 4, TPW = NCT / CG;  // channel tiles per wave
-    static_assert(TPW >= 1 && NCT % CG == 0, "dy_kernel takes C = 64, 128, 256");
-    constexpr int WSTR = C + kLdsPad;         // weight stage row stride (elements)
+    constexpr int NCT = CW / 32, CG = NW / 4, TPW = NCT / CG;  // channel tiles per wave
+    static_assert(TPW >= 1 && NCT % CG == 0 && C % CW == 0, "dy_kernel takes C = 64, 128, 256");
+    constexpr int WSTR = CW + kLdsPad;        // weight stage row stride (elements)
     // dout stage row stride: 36 dwords, so 16 lanes on 16 consecutive rows and
     // one 16-byte column hit 16 distinct groups of four banks
     constexpr int ASTR = KC + 8;
     constexpr int NA = TM * KC / 8 / NT;      // dout 16-byte chunks per thread and stage
-    constexpr int NWL = KC * C / 8 / NT;      // weight 16-byte chunks per thread and stage
+    constexpr int NWL = KC * CW / 8 / NT;     // weight 16-byte chunks per thread and stage
     constexpr int OSTR = 40;                  // staging row stride (elements) of a 32x32 output tile
     constexpr int LW = KC * WSTR, LA = TM * ASTR;
     constexpr int LT = 2 * (LW + LA), LS = NW * 32 * OSTR;
-    static_assert(NA >= 1 && NWL >= 1 && NA * NT == TM * KC / 8 && NWL * NT == KC * C / 8, "stage split");
+    static_assert(NA >= 1 && NWL >= 1 && NA * NT == TM * KC / 8 && NWL * NT == KC * CW / 8, "stage split");
     __shared__ __attribute__((aligned(16))) uint16_t lds[LT > LS ? LT : LS];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -110,6 +112,7 @@ __global__ __launch_bounds__(DyCfg<C>::NT) void dy_kernel(PjBwdArgs a, void *__r
     const int F = a.P * a.HD;
     const int NS = (F + KC - 1) / KC;
     const rsrc_t rW = make_buf(a.W, (uint32_t)F * C * 2u);
+    const int c0 = blockIdx.y * CW;          // first channel of this workgroup
 
     // dout chunk j of this thread: k32 step (half) hf of the stage, token row
     // r, 16-byte column c4; a wave covers 16 rows x 4 columns of one half
@@ -166,8 +169,8 @@ __global__ __launch_bounds__(DyCfg<C>::NT) void dy_kernel(PjBwdArgs a, void *__r
 #pragma unroll
         for (int j = 0; j < NWL; ++j) {  // weight rows s*KC .. (rows past F read as zeros)
             const int idx = tid + j * NT;
-            const int rr = idx / (C / 8), c8 = idx % (C / 8);
-            rw[j] = bload16(rW, (uint32_t)((s * KC + rr) * C + c8 * 8) * 2u);
+            const int rr = idx / (CW / 8), c8 = idx % (CW / 8);
+            rw[j] = bload16(rW, (uint32_t)((s * KC + rr) * C + c0 + c8 * 8) * 2u);
         }
     };
     auto store_stage = [&](int buf, const u32x4 (&ra)[NA], const u32x4 (&rw)[NWL]) {
@@ -179,7 +182,7 @@ __global__ __launch_bounds__(DyCfg<C>::NT) void dy_kernel(PjBwdArgs a, void *__r
 #pragma unroll
         for (int j = 0; j < NWL; ++j) {
             const int idx = tid + j * NT;
-            const int rr = idx / (C / 8), c8 = idx % (C / 8);
+            const int rr = idx / (CW / 8), c8 = idx % (CW / 8);
             *(u32x4 *)&wl[rr * WSTR + c8 * 8] = rw[j];
         }
     };
@@ -235,7 +238,7 @@ __global__ __launch_bounds__(DyCfg<C>::NT) void dy_kernel(PjBwdArgs a, void *__r
         for (int q = 0; q < 2; ++q) {
             const int t = q * 16 + (lane >> 2), c4 = lane & 3;
             const u32x4 v = *(const u32x4 *)&st[t * OSTR + c4 * 8];
-            bstore16(v, rd, (uint32_t)((tb * 32 + t) * C + ct * 32 + c4 * 8) * 2u);
+            bstore16(v, rd, (uint32_t)((tb * 32 + t) * C + c0 + ct * 32 + c4 * 8) * 2u);
         }
         __builtin_amdgcn_wave_barrier();
     }
@@ -468,7 +471,18 @@ hipError_t launch_c(const PjBwdArgs &a, void *ws, const PjBwdPlan &plan, hipStre
     char *w = (char *)ws;
     void *dy = w + plan.off_dy;
     const int64_t nt = (a.R + 127) / 128;
-    hipLaunchKernelGGL((dy_kernel<C>), dim3((unsigned)nt), dim3(DyCfg<C>::NT), 0, s, a, dy);
+    // split the channels when the token blocks alone leave CUs idle
+    int ncs = 1;
+    while (ncs < C / 64 && nt * ncs < 256) ncs *= 2;
+    if (C >= 256 && ncs == 4) {
+        hipLaunchKernelGGL((dy_kernel<C, C / 4 >= 64 ? C / 4 : 64>), dim3((unsigned)nt, 4), dim3(DyCfg<64>::NT), 0, s,
+                           a, dy);
+    } else if (C >= 128 && ncs == 2) {
+        hipLaunchKernelGGL((dy_kernel<C, C / 2 >= 64 ? C / 2 : 64>), dim3((unsigned)nt, 2),
+                           dim3(DyCfg<(C / 2 >= 64 ? C / 2 : 64)>::NT), 0, s, a, dy);
+    } else {
+        hipLaunchKernelGGL((dy_kernel<C, C>), dim3((unsigned)nt), dim3(DyCfg<C>::NT), 0, s, a, dy);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     // LayerNorm backward of dY (bf16) -> dx, dln_w, dln_b
@@ -521,6 +535,11 @@ PjBwdPlan plan_proj_bwd(int64_t R, int C, int HD, int P) {
     // mean fewer partial sums to write and add up; chunks of whole 32-token
     // sub-blocks
     int64_t nch = (proj_bwd_dw_wgs() + nfb - 1) / nfb;
+    // chunks of at least 256 tokens: at few tokens the partial sums would
+    // otherwise cost more traffic than the inputs (at 4096 tokens x 256
+    // channels, 256-token chunks measured 11.2 us, 512-token chunks 12.8)
+    const int64_t nmax = R / 256 > 0 ? R / 256 : 1;
+    if (nch > nmax) nch = nmax;
     const int64_t cap = ((int64_t)1 << 30) / ((int64_t)F * C * 4);  // partials below 1 GiB
     if (nch > cap) nch = cap > 0 ? cap : 1;
     const int64_t nsub = (R + 31) / 32;

@@ -7,6 +7,9 @@
   bias;
 * structure: n_proj projections equal one projection with the stacked
   weight, split; rows are independent; the output is linear in the weight.
+* backward: torch-CPU fp64 autograd through layer_norm + linear; central
+  finite differences; zero / linear in the upstream gradients, per-row
+  channel sums of dx vanish, dbias = column sums, per-projection locality.
 """
 import numpy as np
 import pytest
@@ -120,3 +123,29 @@ def test_backward_finite_differences():
             a2[i] -= h
             num[i] = ((loss(a1, W) - loss(a2, W)) if which == 0 else (loss(x, a1) - loss(x, a2))) / (2 * h)
         np.testing.assert_allclose(grad, num, rtol=1e-6, atol=1e-7)
+
+
+def test_backward_structure():
+    """Zero upstream gradient gives zero gradients; every gradient is linear
+    in the upstream gradients; the input gradient of each row sums to zero
+    over the channels (the LayerNorm removes the row mean); dbias is the
+    column sum of the upstream gradient; a gradient on one projection only
+    touches that projection's weight rows."""
+    x, lw, lb, W, b = _case(12, R=7, C=16, HD=8, P=3)
+    rng = np.random.default_rng(13)
+    d1 = [rng.standard_normal((7, 8)) for _ in range(3)]
+    d2 = [rng.standard_normal((7, 8)) for _ in range(3)]
+    zero = oracle.ln_proj_backward(x, lw, lb, W, [np.zeros((7, 8))] * 3)
+    for g in zero:
+        assert np.abs(g).max() == 0.0
+    g1 = oracle.ln_proj_backward(x, lw, lb, W, d1)
+    g2 = oracle.ln_proj_backward(x, lw, lb, W, d2)
+    g12 = oracle.ln_proj_backward(x, lw, lb, W, [2.0 * a - 3.0 * c for a, c in zip(d1, d2)])
+    for a, c, ac in zip(g1, g2, g12):
+        np.testing.assert_allclose(ac, 2.0 * a - 3.0 * c, rtol=1e-11, atol=1e-11)
+    np.testing.assert_allclose(g1[0].sum(axis=1), 0.0, atol=1e-12)
+    np.testing.assert_allclose(g1[4], np.concatenate([d.sum(axis=0) for d in d1]), rtol=1e-13, atol=1e-13)
+    only1 = oracle.ln_proj_backward(x, lw, lb, W, [np.zeros((7, 8)), d1[1], np.zeros((7, 8))])
+    dW = only1[3]
+    assert np.abs(dW[:8]).max() == 0.0 and np.abs(dW[16:]).max() == 0.0
+    assert np.abs(dW[8:16]).max() > 0.0

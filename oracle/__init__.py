@@ -223,6 +223,35 @@ def pair_bias_forward(z, ln_weight, ln_bias, weight, eps: float = 1e-5, transpos
     return np.ascontiguousarray(out)
 
 
+def pair_bias_backward(z, ln_weight, ln_bias, weight, dbias, eps: float = 1e-5, transpose: bool = False):
+    """Gradients of pair_bias_forward for the upstream gradient dbias (the
+    attention backward's dL/dbias, [B, H, Li, Lj], or [B, H, Lj, Li] with
+    transpose): (dz, dln_weight, dln_bias, dweight [H, C]).
+
+    With y = LN(z) and g[b, i, j, h] the upstream value of entry (i, j):
+    dY = g @ W;  (dz, dln_weight, dln_bias) is the LayerNorm backward of dY;
+    dW = sum over entries of g^T y.  Matmuls are library primitives (numpy,
+    fp64)."""
+    z = _f64(z)
+    W = _f64(weight)
+    g = _f64(dbias)
+    if z.ndim != 4 or W.ndim != 2 or W.shape[1] != z.shape[3]:
+        raise ValueError("z is [B, Li, Lj, C] and weight [H, C]")
+    B, Li, Lj, C = z.shape
+    H = W.shape[0]
+    want = (B, H, Lj, Li) if transpose else (B, H, Li, Lj)
+    if g.shape != want:
+        raise ValueError("dbias must be %s" % (want,))
+    if transpose:
+        g = np.swapaxes(g, 2, 3)                 # [B, H, Li, Lj]
+    g = np.moveaxis(g, 1, 3)                     # [B, Li, Lj, H]
+    y, _, _ = layernorm_forward(z, ln_weight, ln_bias, eps)
+    dY = g @ W                                   # [B, Li, Lj, C]
+    dz, dlw, dlb = layernorm_backward(z, dY, ln_weight, eps)
+    dW = g.reshape(-1, H).T @ y.reshape(-1, C)   # [H, C]
+    return dz, dlw, dlb, dW
+
+
 def ln_proj_backward(x, ln_weight, ln_bias, weight, douts, eps: float = 1e-5):
     """Gradients of ln_proj_forward for upstream gradients douts[p] ([..., HD]):
     (dx, dln_weight, dln_bias, dweight [n_proj*HD, C], dbias [n_proj*HD]).

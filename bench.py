@@ -579,6 +579,32 @@ def pair_bias_bench(torch, args):
         torch.cuda.synchronize()
         res[mode] = [a.elapsed_time(b_) for a, b_ in ev]
     del flush
+    # backward from an fp32 dbias in the forward's layout: dz, dweight, dln
+    gen = torch.Generator(device="cpu").manual_seed(w.seed + 1)
+    gshape = (w.n_batch, H, L, L)  # square: the same shape in either layout
+    g = torch.randn(gshape, generator=gen).cuda()
+    C = w.c_in
+    bbufs = dict(dz=torch.empty_like(z), dweight=torch.empty(H, C, device="cuda"),
+                 dln_weight=torch.empty(C, device="cuda"), dln_bias=torch.empty(C, device="cuda"),
+                 workspace=torch.empty(max(16, pj.pair_bias_bwd_workspace_size(w.n_batch, L, L, C, H, w.transpose)),
+                                       dtype=torch.uint8, device="cuda"))
+
+    def bwd():
+        pj.ln_pair_bias_bwd(z, lnw, lnb, Wt, g, w.eps, w.transpose, stream=stream, **bbufs)
+
+    for _ in range(args.warmup):
+        bwd()
+    torch.cuda.synchronize()
+    bev = [(mk(), mk()) for _ in range(args.steps)]
+    for a_, b2 in bev:
+        a_.record(stream)
+        bwd()
+        b2.record(stream)
+    torch.cuda.synchronize()
+    bwd_ms = [a_.elapsed_time(b2) for a_, b2 in bev]
+    # algorithmic bytes: read z and dbias, write dz, partial rows out and back
+    n_ent = w.n_batch * L * L
+    bwd_bytes = 4 * n_ent * C + 4 * n_ent * H + 2 * bbufs["workspace"].numel()
     k_ms = float(np.mean(res["warm"]))
     nbytes = w.bytes()
     ach = nbytes / (k_ms * 1e-3) / 1e9
@@ -606,6 +632,8 @@ def pair_bias_bench(torch, args):
     line = {
         "metric": "Pair bias (LayerNorm + projection to heads, attention layout), GB/s on 1 MI355X",
         "value": round(nbytes / (ms_step * 1e-3) / 1e9, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "bwd_ms": _pct(bwd_ms), "bwd_algorithmic_bytes": int(bwd_bytes),
+        "bwd_gbs": round(bwd_bytes / (float(np.median(bwd_ms)) * 1e-3) / 1e9, 1),
         "warmup": args.warmup, "ms_per_step": round(ms_step, 5), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": w.name, "n_batch": w.n_batch, "seq_len": L, "c_in": w.c_in, "n_heads": H,
@@ -871,6 +899,7 @@ KERNEL_SOURCES = {"attn": ("evo_frag.h", "evo_fwd.hip", "evo_bwd.hip"),
                   "proj": ("evo_frag.h", "evo_proj.hip"),
                   "proj_bwd": ("evo_frag.h", "evo_proj_bwd.hip"),
                   "pb": ("evo_frag.h", "evo_pair_bias.hip"),
+                  "pb_bwd": ("evo_frag.h", "evo_pair_bias_bwd.hip"),
                   "optim": ("evo_frag.h", "evo_optim.hip")}
 
 
@@ -879,6 +908,8 @@ def kernel_family(kernel: str) -> str:
         return "proj"
     if kernel in ("dy_kernel", "dw_kernel", "colsum_kernel"):
         return "proj_bwd"
+    if kernel in ("pair_bias_bwd_kernel", "pb_param_reduce_kernel"):
+        return "pb_bwd"
     if kernel.startswith("pair_bias"):
         return "pb"
     if kernel in ("adam_swa_kernel", "sumsq_kernel", "clip_scale_kernel"):

@@ -125,6 +125,33 @@ int evo_ln_pair_bias_fwd(const evo_pair_bias_dims *dims, const void *z, const fl
                          const float *ln_bias, const void *weight, void *out, float *mean, float *rstd,
                          void *stream);
 
+/* Backward of evo_ln_pair_bias_fwd (ScaleFold Section 3.3, the pair-bias term
+ * of the attention, differentiated): given the attention backward's
+ * dL/dbias g, in the forward's output layout (fp32 [B, H, Li, Lj], or
+ * [B, H, Lj, Li] with transpose), and y = LayerNorm(z[b, i, j, :]) as above,
+ *
+ *   dY[b,i,j,c] = sum_h g[b,h,i,j] weight[h,c]
+ *   dz          = LayerNorm backward of dY               (bf16 [B, Li, Lj, C])
+ *   dweight     = sum over (b,i,j) of g[b,h,i,j] y[c]    (fp32 [H, C])
+ *   dln_weight  = sum over (b,i,j) of dY * xhat,  dln_bias = sum of dY   (fp32 [C])
+ *
+ * The statistics are recomputed from z (the forward's are not needed).  All
+ * sums run in a fixed order: repeated calls give identical bits.
+ * dbias: contiguous fp32, 16-byte aligned; dz: contiguous bf16 like z,
+ * 16-byte aligned, not aliasing z; dweight, dln_weight, dln_bias: fp32,
+ * 16-byte aligned, distinct.  workspace: device memory of at least
+ * evo_ln_pair_bias_bwd_workspace_size(dims) bytes, 16-byte aligned (nullable
+ * when that size is 0), overwritten.  Compiled set: as the forward, with
+ * H in {1, 2, 4, 8}.  B, Li or Lj == 0 validates and returns EVO_OK without
+ * touching any pointer.  Errors: EVO_ERR_INVALID_ARG (null or aliasing
+ * pointers, bad dims), EVO_ERR_UNSUPPORTED (outside the compiled set),
+ * EVO_ERR_ALIGNMENT, EVO_ERR_WORKSPACE (too small), EVO_ERR_HIP (launch). */
+size_t evo_ln_pair_bias_bwd_workspace_size(const evo_pair_bias_dims *dims);
+int evo_ln_pair_bias_bwd(const evo_pair_bias_dims *dims, const void *z, const float *ln_weight,
+                         const float *ln_bias, const void *weight, const float *dbias, void *dz,
+                         float *dweight, float *dln_weight, float *dln_bias, void *workspace,
+                         size_t workspace_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

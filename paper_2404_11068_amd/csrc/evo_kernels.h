@@ -141,6 +141,25 @@ struct PbArgs {
 bool pair_bias_supported(int C, int H);
 hipError_t launch_pair_bias(const PbArgs &a, hipStream_t s);
 
+// backward of the pair bias: dz, dW [H, C], dln_w, dln_b from dbias (fp32,
+// the forward's output layout)
+struct PbBwdArgs {
+    const void *z;            // [B, Li, Lj, C] bf16
+    const float *lnw, *lnb;   // [C]
+    const void *W;            // [H, C] bf16
+    const float *dbias;       // [B, H, Li, Lj] (or [B, H, Lj, Li] when transpose) fp32
+    void *dz;                 // [B, Li, Lj, C] bf16
+    float *dW, *dlnw, *dlnb;  // [H, C], [C], [C]
+    int64_t B;
+    int Li, Lj, C, H, transpose;
+    float eps;
+};
+
+bool pair_bias_bwd_supported(int C, int H);
+int64_t pair_bias_bwd_workgroups(int64_t B, int Li, int Lj, int C);
+size_t pair_bias_bwd_workspace(int64_t B, int Li, int Lj, int C, int H);
+hipError_t launch_pair_bias_bwd(const PbBwdArgs &a, void *ws, hipStream_t s);
+
 bool proj_supported(int C, int HD, int P);
 hipError_t launch_ln_proj(const PjArgs &a, hipStream_t s);
 

@@ -126,18 +126,27 @@ int evo_ln_proj_bwd(const evo_proj_dims *d, const void *x, const float *ln_weigh
     return evo::launch_ln_proj_bwd(a, workspace, plan, (hipStream_t)stream) == hipSuccess ? EVO_OK : EVO_ERR_HIP;
 }
 
-int evo_ln_pair_bias_fwd(const evo_pair_bias_dims *d, const void *z, const float *ln_weight, const float *ln_bias,
-                         const void *weight, void *out, float *mean, float *rstd, void *stream) {
+// dims shared by the pair-bias forward and backward; `bwd` also requires the
+// backward's compiled head counts and its fp32 gradient plane below 2^31 bytes
+static int check_pb(const evo_pair_bias_dims *d, bool bwd) {
     if (!d || d->reserved != 0) return EVO_ERR_INVALID_ARG;
     if (d->dtype != EVO_DTYPE_BF16) return EVO_ERR_UNSUPPORTED;
     if (d->n_batch < 0 || d->len_i < 0 || d->len_j < 0 || d->c_in < 1 || d->n_heads < 1 ||
         (d->transpose != 0 && d->transpose != 1) || !(d->eps >= 0.0f) || !isfinite(d->eps))
         return EVO_ERR_INVALID_ARG;
-    if (!evo::pair_bias_supported(d->c_in, d->n_heads)) return EVO_ERR_UNSUPPORTED;
+    if (!(bwd ? evo::pair_bias_bwd_supported(d->c_in, d->n_heads) : evo::pair_bias_supported(d->c_in, d->n_heads)))
+        return EVO_ERR_UNSUPPORTED;
     if (d->len_i % 8 != 0 || d->len_j % 8 != 0) return EVO_ERR_UNSUPPORTED;
-    if ((int64_t)d->n_heads * d->len_i * d->len_j * 2 >= 0x7fffffffLL ||
+    if ((int64_t)d->n_heads * d->len_i * d->len_j * (bwd ? 4 : 2) >= 0x7fffffffLL ||
         d->len_j * d->c_in * 2 >= 0x7fffffffLL || d->n_batch > 65535)
         return EVO_ERR_UNSUPPORTED;
+    return EVO_OK;
+}
+
+int evo_ln_pair_bias_fwd(const evo_pair_bias_dims *d, const void *z, const float *ln_weight, const float *ln_bias,
+                         const void *weight, void *out, float *mean, float *rstd, void *stream) {
+    const int st = check_pb(d, false);
+    if (st) return st;
     if (d->n_batch == 0 || d->len_i == 0 || d->len_j == 0) return EVO_OK;
     if (!z || !ln_weight || !ln_bias || !weight || !out || out == z) return EVO_ERR_INVALID_ARG;
     if ((mean == nullptr) != (rstd == nullptr) || (mean && (void *)mean == (void *)rstd)) return EVO_ERR_INVALID_ARG;
@@ -160,6 +169,48 @@ int evo_ln_pair_bias_fwd(const evo_pair_bias_dims *d, const void *z, const float
     a.transpose = d->transpose;
     a.eps = d->eps;
     return evo::launch_pair_bias(a, (hipStream_t)stream) == hipSuccess ? EVO_OK : EVO_ERR_HIP;
+}
+
+size_t evo_ln_pair_bias_bwd_workspace_size(const evo_pair_bias_dims *d) {
+    if (check_pb(d, true) || d->n_batch == 0 || d->len_i == 0 || d->len_j == 0) return 0;
+    return evo::pair_bias_bwd_workspace(d->n_batch, (int)d->len_i, (int)d->len_j, d->c_in, d->n_heads);
+}
+
+int evo_ln_pair_bias_bwd(const evo_pair_bias_dims *d, const void *z, const float *ln_weight, const float *ln_bias,
+                         const void *weight, const float *dbias, void *dz, float *dweight, float *dln_weight,
+                         float *dln_bias, void *workspace, size_t workspace_bytes, void *stream) {
+    const int st = check_pb(d, true);
+    if (st) return st;
+    if (d->n_batch == 0 || d->len_i == 0 || d->len_j == 0) return EVO_OK;
+    if (!z || !ln_weight || !ln_bias || !weight || !dbias || !dz || !dweight || !dln_weight || !dln_bias)
+        return EVO_ERR_INVALID_ARG;
+    if (dz == z || (const void *)dz == (const void *)dbias || dweight == dln_weight || dweight == dln_bias ||
+        dln_weight == dln_bias)
+        return EVO_ERR_INVALID_ARG;
+    const void *al16[] = {z, ln_weight, ln_bias, weight, dbias, dz, dweight, dln_weight, dln_bias};
+    for (const void *p : al16)
+        if (!aligned(p, 16)) return EVO_ERR_ALIGNMENT;
+    const size_t need = evo::pair_bias_bwd_workspace(d->n_batch, (int)d->len_i, (int)d->len_j, d->c_in, d->n_heads);
+    if (!workspace || workspace_bytes < need) return EVO_ERR_WORKSPACE;
+    if (!aligned(workspace, 16)) return EVO_ERR_ALIGNMENT;
+    evo::PbBwdArgs a{};
+    a.z = z;
+    a.lnw = ln_weight;
+    a.lnb = ln_bias;
+    a.W = weight;
+    a.dbias = dbias;
+    a.dz = dz;
+    a.dW = dweight;
+    a.dlnw = dln_weight;
+    a.dlnb = dln_bias;
+    a.B = d->n_batch;
+    a.Li = (int)d->len_i;
+    a.Lj = (int)d->len_j;
+    a.C = d->c_in;
+    a.H = d->n_heads;
+    a.transpose = d->transpose;
+    a.eps = d->eps;
+    return evo::launch_pair_bias_bwd(a, workspace, (hipStream_t)stream) == hipSuccess ? EVO_OK : EVO_ERR_HIP;
 }
 
 }  // extern "C"

@@ -141,6 +141,10 @@ def _pb_lib():
     if not _pb_bound:
         P = ctypes.c_void_p
         lib.evo_ln_pair_bias_fwd.argtypes = [ctypes.POINTER(evo_pair_bias_dims)] + [P] * 8
+        lib.evo_ln_pair_bias_bwd_workspace_size.argtypes = [ctypes.POINTER(evo_pair_bias_dims)]
+        lib.evo_ln_pair_bias_bwd_workspace_size.restype = ctypes.c_size_t
+        lib.evo_ln_pair_bias_bwd.argtypes = [ctypes.POINTER(evo_pair_bias_dims)] + [P] * 10 + [ctypes.c_size_t, P]
+        lib.evo_ln_pair_bias_bwd.restype = ctypes.c_int
         lib.evo_ln_pair_bias_fwd.restype = ctypes.c_int
         _pb_bound = True
     return lib
@@ -178,3 +182,51 @@ def ln_pair_bias_fwd(z: torch.Tensor, ln_weight: torch.Tensor, ln_bias: torch.Te
     if st:
         raise EvoAttnError(st, "evo_ln_pair_bias_fwd")
     return (out, mean, rstd) if need_stats else out
+
+
+def pair_bias_bwd_workspace_size(B: int, Li: int, Lj: int, C: int, H: int, transpose: bool = False,
+                                 eps: float = 1e-5) -> int:
+    d = evo_pair_bias_dims(EVO_DTYPE_BF16, C, H, 1 if transpose else 0, B, Li, Lj, float(eps), 0)
+    return int(_pb_lib().evo_ln_pair_bias_bwd_workspace_size(ctypes.byref(d)))
+
+
+def ln_pair_bias_bwd(z: torch.Tensor, ln_weight: torch.Tensor, ln_bias: torch.Tensor, weight: torch.Tensor,
+                     dbias: torch.Tensor, eps: float = 1e-5, transpose: bool = False, *,
+                     dz: Optional[torch.Tensor] = None, dweight: Optional[torch.Tensor] = None,
+                     dln_weight: Optional[torch.Tensor] = None, dln_bias: Optional[torch.Tensor] = None,
+                     workspace: Optional[torch.Tensor] = None, stream=None):
+    """Gradients (dz, dweight [H, C], dln_weight, dln_bias) of ln_pair_bias_fwd
+    for the upstream gradient dbias (fp32, the forward's output layout)."""
+    lib = _pb_lib()
+    if z.dim() == 3:
+        z = z.unsqueeze(0)
+    if z.dtype != torch.bfloat16 or weight.dtype != torch.bfloat16 or not z.is_contiguous() \
+            or not weight.is_contiguous():
+        raise ValueError("z and weight must be contiguous bfloat16")
+    B, Li, Lj, C = z.shape
+    H = weight.shape[0]
+    if weight.shape != (H, C):
+        raise ValueError("weight must be [H, C]")
+    shape = (B, H, Lj, Li) if transpose else (B, H, Li, Lj)
+    if dbias.dim() == 3:
+        dbias = dbias.unsqueeze(0)
+    if tuple(dbias.shape) != shape or dbias.dtype != torch.float32 or not dbias.is_contiguous():
+        raise ValueError("dbias must be a contiguous float32 tensor of shape %s" % (shape,))
+    dz = torch.empty_like(z) if dz is None else dz
+    if dz.shape != z.shape or dz.dtype != torch.bfloat16 or not dz.is_contiguous():
+        raise ValueError("dz must be contiguous and shaped like z")
+    f32 = lambda n: torch.empty(n, dtype=torch.float32, device=z.device)
+    dweight = f32((H, C)) if dweight is None else dweight
+    dln_weight = f32(C) if dln_weight is None else dln_weight
+    dln_bias = f32(C) if dln_bias is None else dln_bias
+    d = evo_pair_bias_dims(EVO_DTYPE_BF16, C, H, 1 if transpose else 0, B, Li, Lj, float(eps), 0)
+    need = int(lib.evo_ln_pair_bias_bwd_workspace_size(ctypes.byref(d)))
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=z.device)
+    st = lib.evo_ln_pair_bias_bwd(ctypes.byref(d), _ptr(z), _ptr(ln_weight), _ptr(ln_bias), _ptr(weight),
+                                  _ptr(dbias), _ptr(dz), _ptr(dweight), _ptr(dln_weight), _ptr(dln_bias),
+                                  _ptr(workspace), ctypes.c_size_t(workspace.numel() * workspace.element_size()),
+                                  _stream(stream))
+    if st:
+        raise EvoAttnError(st, "evo_ln_pair_bias_bwd")
+    return dz, dweight, dln_weight, dln_bias

@@ -58,3 +58,56 @@ def test_rejects_bad_pointers():
 
 def test_empty_needs_no_pointers():
     assert _call(_dims(len_i=0), z=None, lnw=None, lnb=None, w=None, out=None) == 0
+
+
+# ---- backward ---------------------------------------------------------------
+
+def _call_bwd(dims, z=FAKE, lnw=FAKE + 0x1000000, lnb=FAKE + 0x1001000, w=FAKE + 0x1002000, g=FAKE + 0x3000000,
+              dz=FAKE + 0x5000000, dw=FAKE + 0x7000000, dlw=FAKE + 0x7100000, dlb=FAKE + 0x7200000,
+              ws=FAKE + 0x8000000, ws_bytes=1 << 30):
+    return _lib().evo_ln_pair_bias_bwd(ctypes.byref(dims) if dims is not None else None, P(z), P(lnw), P(lnb),
+                                       P(w), P(g), P(dz), P(dw), P(dlw), P(dlb), P(ws), ctypes.c_size_t(ws_bytes),
+                                       None)
+
+
+def test_bwd_exported():
+    lib = _lib()
+    assert hasattr(lib, "evo_ln_pair_bias_bwd") and hasattr(lib, "evo_ln_pair_bias_bwd_workspace_size")
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=0), 2), (dict(c_in=96), 2), (dict(n_heads=3), 2), (dict(n_heads=16), 2),
+    (dict(len_i=250), 2), (dict(len_j=12), 2), (dict(transpose=2), 1), (dict(n_batch=-1), 1),
+    (dict(eps=-1.0), 1), (dict(reserved=7), 1), (dict(n_heads=0), 1),
+    (dict(len_i=1 << 14, len_j=1 << 14), 2),
+])
+def test_bwd_rejects_bad_dims(kw, status):
+    d = _dims(**kw)
+    assert _call_bwd(d) == status
+    assert _lib().evo_ln_pair_bias_bwd_workspace_size(ctypes.byref(d)) == 0
+
+
+def test_bwd_rejects_bad_pointers_and_workspace():
+    d = _dims()
+    need = _lib().evo_ln_pair_bias_bwd_workspace_size(ctypes.byref(d))
+    # one partial row (H*C + 2C floats) per workgroup, at most 512 workgroups
+    assert need == 512 * (8 * 128 + 2 * 128) * 4
+    assert _call_bwd(None) == 1
+    for k in ("z", "lnw", "lnb", "w", "g", "dz", "dw", "dlw", "dlb"):
+        assert _call_bwd(d, **{k: None}) == 1, k
+    assert _call_bwd(d, dz=FAKE) == 1                      # dz aliases z
+    assert _call_bwd(d, dlw=FAKE + 0x7000000) == 1         # dln_weight aliases dweight
+    assert _call_bwd(d, dlb=FAKE + 0x7100000) == 1         # dln_bias aliases dln_weight
+    assert _call_bwd(d, z=FAKE + 8) == 3
+    assert _call_bwd(d, g=FAKE + 0x3000004) == 3
+    assert _call_bwd(d, dw=FAKE + 0x7000004) == 3
+    assert _call_bwd(d, ws=None) == 4
+    assert _call_bwd(d, ws_bytes=need - 1) == 4
+    assert _call_bwd(d, ws=FAKE + 0x8000008) == 3
+
+
+def test_bwd_empty_needs_no_pointers():
+    d = _dims(len_j=0)
+    assert _lib().evo_ln_pair_bias_bwd_workspace_size(ctypes.byref(d)) == 0
+    assert _call_bwd(d, z=None, lnw=None, lnb=None, w=None, g=None, dz=None, dw=None, dlw=None, dlb=None,
+                     ws=None, ws_bytes=0) == 0

@@ -26,7 +26,8 @@ def test_exports_declared_symbol():
     decls = re.findall(r"^\s*(?:int|size_t)\s*(evo_\w+)\s*\(",
                        open(os.path.join(ROOT, "include", "evo_proj.h")).read(), flags=re.M)
     assert set(decls) == {"evo_ln_proj_fwd", "evo_ln_proj_fwd_ex", "evo_ln_proj_bwd_workspace_size",
-                          "evo_ln_proj_bwd", "evo_ln_pair_bias_fwd"}
+                          "evo_ln_proj_bwd", "evo_ln_pair_bias_fwd", "evo_ln_pair_bias_bwd_workspace_size",
+                          "evo_ln_pair_bias_bwd"}
     for name in decls:
         assert hasattr(lib, name), name
 

@@ -100,7 +100,8 @@ class GraphCache:
 
 class MSARowAttentionStep:
     """Static buffers and weights of one MSA row attention with pair bias:
-    m [N, L, c_m], z [L, L, c_z] -> q, k, v, g, bias -> o, lse -> dq, dk, dv, dg, dbias."""
+    m [N, L, c_m], z [L, L, c_z] -> q, k, v, g, bias -> o, lse -> dq, dk, dv, dg, dbias -> dm and the
+    projection weight gradients, dz and the pair-bias weight gradients."""
 
     def __init__(self, N: int, L: int, c_m: int = 256, c_z: int = 128, H: int = 8, d: int = 32, seed: int = 0,
                  device="cuda"):
@@ -137,6 +138,13 @@ class MSARowAttentionStep:
         dims = pj.evo_proj_dims(1, c_m, 4, H * d, N * L, 1e-5, 0)
         self.ws_proj = torch.empty(max(int(pj._lib().evo_ln_proj_bwd_workspace_size(ctypes.byref(dims))), 1),
                                    dtype=torch.uint8, device=device)
+        # pair-bias gradients (the attention's dbias through LN(z) and the projection to heads)
+        self.dz = torch.empty_like(self.z)
+        self.dw_bias = torch.empty(H, c_z, **f32)
+        self.dln_z_w = torch.empty(c_z, **f32)
+        self.dln_z_b = torch.empty(c_z, **f32)
+        self.ws_pb = torch.empty(max(pj.pair_bias_bwd_workspace_size(1, L, L, c_z, H), 16), dtype=torch.uint8,
+                                 device=device)
 
         self._key = hash((N, L, H, d, self.m.data_ptr(), self.z.data_ptr(), self.dq.data_ptr())) & \
             0xFFFFFFFFFFFFFFFF
@@ -146,7 +154,7 @@ class MSARowAttentionStep:
         return self._key
 
     def record(self, stream):
-        """Enqueue the step (5 C-ABI calls, 14 kernels) on `stream` (torch stream or raw handle)."""
+        """Enqueue the step (6 C-ABI calls, 16 kernels) on `stream` (torch stream or raw handle)."""
         pj.ln_proj_fwd(self.m, self.ln_m_w, self.ln_m_b, self.w_qkvg, self.b_qkvg, n_proj=4,
                        outs=[t.view(self.N, self.L, -1) for t in (self.q, self.k, self.v, self.gate)],
                        mean=self.mean, rstd=self.rstd, y_norm=self.y_norm, stream=stream)
@@ -160,7 +168,11 @@ class MSARowAttentionStep:
                        [t.view(self.N, self.L, -1) for t in (self.dq, self.dk, self.dv, self.dg)],
                        dx=self.dm, dweight=self.dw_qkvg, dbias=self.db_qkvg, dln_weight=self.dln_m_w,
                        dln_bias=self.dln_m_b, workspace=self.ws_proj, stream=stream)
+        pj.ln_pair_bias_bwd(self.z, self.ln_z_w, self.ln_z_b, self.w_bias, self.dbias, dz=self.dz,
+                            dweight=self.dw_bias, dln_weight=self.dln_z_w, dln_bias=self.dln_z_b, workspace=self.ws_pb,
+                            stream=stream)
 
     def outputs(self):
         return {k: getattr(self, k) for k in ("q", "k", "v", "gate", "bias", "out", "lse", "dq", "dk", "dv", "dg",
-                                               "dbias", "y_norm", "dm", "dw_qkvg", "db_qkvg", "dln_m_w", "dln_m_b")}
+                                               "dbias", "y_norm", "dm", "dw_qkvg", "db_qkvg", "dln_m_w", "dln_m_b",
+                                               "dz", "dw_bias", "dln_z_w", "dln_z_b")}

@@ -1,5 +1,6 @@
 """GPU checks of the HIP graph cache on an MSA-row-attention step
-(LayerNorm + projections, pair bias, attention forward and backward).
+(LayerNorm + projections, pair bias, attention forward and backward, and the
+backward of the projections and of the pair bias).
 
 * a replayed graph gives bitwise the results of the same step run eagerly
   (every kernel is deterministic), over several replays with new input

@@ -223,6 +223,42 @@ def pair_bias_forward(z, ln_weight, ln_bias, weight, eps: float = 1e-5, transpos
     return np.ascontiguousarray(out)
 
 
+def linear_forward(x, weight, bias=None, n_proj: int = 1):
+    """n_proj linear layers sharing the input x [..., C]: outs[p] = x W_p^T + b_p
+    with W_p = weight[p*HD:(p+1)*HD] (torch Linear layout) -- the output
+    projection after the gated attention, and the batched projections of
+    ln_proj_forward without their LayerNorm.  numpy matmul, fp64."""
+    x = _f64(x)
+    W = _f64(weight)
+    if W.ndim != 2 or W.shape[1] != x.shape[-1] or W.shape[0] % n_proj:
+        raise ValueError("weight must be [n_proj * HD, C]")
+    HD = W.shape[0] // n_proj
+    b = None if bias is None else _f64(bias)
+    outs = []
+    for p in range(n_proj):
+        o = x @ W[p * HD:(p + 1) * HD].T
+        if b is not None:
+            o = o + b[p * HD:(p + 1) * HD]
+        outs.append(o)
+    return outs
+
+
+def linear_backward(x, weight, douts):
+    """Gradients of linear_forward: (dx, dweight [n_proj*HD, C], dbias [n_proj*HD])
+    with dx = sum_p dout_p W_p, dW_p = dout_p^T x, db_p = sum over tokens of dout_p."""
+    x = _f64(x)
+    W = _f64(weight)
+    C = x.shape[-1]
+    P = len(douts)
+    HD = W.shape[0] // P
+    x2 = x.reshape(-1, C)
+    d2 = [_f64(d).reshape(-1, HD) for d in douts]
+    dx = sum(d2[p] @ W[p * HD:(p + 1) * HD] for p in range(P))
+    dW = np.concatenate([d2[p].T @ x2 for p in range(P)], axis=0)
+    db = np.concatenate([d2[p].sum(axis=0) for p in range(P)])
+    return dx.reshape(x.shape), dW, db
+
+
 def pair_bias_backward(z, ln_weight, ln_bias, weight, dbias, eps: float = 1e-5, transpose: bool = False):
     """Gradients of pair_bias_forward for the upstream gradient dbias (the
     attention backward's dL/dbias, [B, H, Li, Lj], or [B, H, Lj, Li] with

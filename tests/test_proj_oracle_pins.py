@@ -149,3 +149,28 @@ def test_backward_structure():
     dW = only1[3]
     assert np.abs(dW[:8]).max() == 0.0 and np.abs(dW[16:]).max() == 0.0
     assert np.abs(dW[8:16]).max() > 0.0
+
+
+def test_linear_matches_torch_forward_and_autograd():
+    """The linear layers (no LayerNorm) against torch linear and autograd; a
+    linear layer on LN(x) is the LayerNorm variant's projection."""
+    x, lw, lb, W, b = _case(30, R=9, C=16, HD=8, P=3)
+    outs = oracle.linear_forward(x, W, b, n_proj=3)
+    xt = torch.tensor(x, requires_grad=True)
+    Wt = torch.tensor(W, requires_grad=True)
+    bt = torch.tensor(b, requires_grad=True)
+    rng = np.random.default_rng(31)
+    douts = [rng.standard_normal((9, 8)) for _ in range(3)]
+    loss = 0.0
+    for p in range(3):
+        ref = F.linear(xt, Wt[p * 8:(p + 1) * 8], bt[p * 8:(p + 1) * 8])
+        np.testing.assert_allclose(outs[p], ref.detach().numpy(), rtol=1e-12, atol=1e-12)
+        loss = loss + (ref * torch.tensor(douts[p])).sum()
+    loss.backward()
+    dx, dW, db = oracle.linear_backward(x, W, douts)
+    np.testing.assert_allclose(dx, xt.grad.numpy(), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(dW, Wt.grad.numpy(), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(db, bt.grad.numpy(), rtol=1e-12, atol=1e-12)
+    y, _, _ = oracle.layernorm_forward(x, lw, lb, 1e-5)
+    for a, c in zip(oracle.linear_forward(y, W, b, n_proj=3), oracle.ln_proj_forward(x, lw, lb, W, b, n_proj=3)):
+        np.testing.assert_allclose(a, c, rtol=1e-13, atol=1e-13)

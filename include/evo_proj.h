@@ -88,6 +88,27 @@ int evo_ln_proj_bwd(const evo_proj_dims *dims, const void *x, const float *ln_we
                     void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * Linear layers without the LayerNorm: the same batched products on x itself,
+ * outs[p] = x @ weight[p*HD:(p+1)*HD, :]^T + bias[p*HD:(p+1)*HD] — the output
+ * projection that follows the gated attention in every Evoformer attention
+ * module (ScaleFold Section 3.3 fuses the module's other linear layers with
+ * its LayerNorm and MHA; this one reads the attention's gated output, [N, L,
+ * H, d] = [R, C] with C = H * d).  dims, layouts and compiled set as above;
+ * eps is unused (still validated).
+ *
+ * Backward: dx = sum_p douts[p] @ weight_p (rounded to bf16, written to dx),
+ * dweight[p*HD + f, c] = sum_t douts[p][t, f] * x[t, c], dbias as above.
+ * workspace: evo_linear_bwd_workspace_size(dims) bytes, 256-byte aligned.
+ * Errors as for the LayerNorm variants; R == 0 returns EVO_OK untouched.
+ */
+int evo_linear_fwd(const evo_proj_dims *dims, const void *x, const void *weight, const float *bias,
+                   void *const *outs, void *stream);
+size_t evo_linear_bwd_workspace_size(const evo_proj_dims *dims);
+int evo_linear_bwd(const evo_proj_dims *dims, const void *x, const void *weight, const void *const *douts,
+                   void *dx, float *dweight, float *dbias, void *workspace, size_t workspace_bytes,
+                   void *stream);
+
+/*
  * Pair bias: the logit bias every pair-biased Evoformer attention adds before
  * its softmax (ScaleFold Section 3.3, "Multi Head Attention"), a LayerNorm of
  * each pair entry followed by a bias-free linear map to one value per head,

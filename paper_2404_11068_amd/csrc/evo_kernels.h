@@ -91,7 +91,7 @@ hipError_t launch_ln_bwd(const LnProblem &p, const LnBwdPtrs &x, void *ws, hipSt
 // LayerNorm + P batched projections (bf16): out_p = LN(x) W_p^T + b_p
 struct PjArgs {
     const void *x;            // [R, C] bf16
-    const float *lnw, *lnb;   // [C]
+    const float *lnw, *lnb;   // [C], or both null for a plain linear layer
     const void *W;            // [P*HD, C] bf16
     const float *bias;        // [P*HD] or null
     void *out0, *out1, *out2, *out3;  // [R, HD] bf16 each (first P used)
@@ -105,9 +105,9 @@ struct PjArgs {
 // backward of the fused LayerNorm + projections
 struct PjBwdArgs {
     const void *x;            // [R, C] bf16
-    const float *lnw;         // [C]
+    const float *lnw;         // [C], or null for a plain linear layer
     const float *mean, *rstd; // [R]
-    const void *y;            // [R, C] bf16 normalised input from the forward
+    const void *y;            // [R, C] bf16 normalised input from the forward (x without LayerNorm)
     const void *W;            // [P*HD, C] bf16
     const void *dout0, *dout1, *dout2, *dout3;  // [R, HD] bf16
     void *dx;                 // [R, C] bf16
@@ -123,7 +123,9 @@ struct PjBwdPlan {
     size_t off_dy, off_ln, off_dw, off_db, total;
 };
 
-PjBwdPlan plan_proj_bwd(int64_t R, int C, int HD, int P);
+// ln == false: a plain linear layer (no LayerNorm; lnw, mean, rstd, dlnw,
+// dlnb null and y = x), dY written straight to dx
+PjBwdPlan plan_proj_bwd(int64_t R, int C, int HD, int P, bool ln = true);
 hipError_t launch_ln_proj_bwd(const PjBwdArgs &a, void *ws, const PjBwdPlan &plan, hipStream_t s);
 
 // LayerNorm of pair entries projected to per-head logit biases (bf16)

@@ -82,7 +82,8 @@ __global__ __launch_bounds__(64 * kPjWaves) void ln_proj_kernel(PjArgs a) {
             const int r = wave * (G::TM / kPjWaves) + s * G::RPW + rs;
             raw[s] = bload16(rx, (uint32_t)(r * C + li * 8) * 2u);
         }
-        const rsrc_t rw = make_buf(a.lnw, C * 4), rb = make_buf(a.lnb, C * 4);
+        // (empty resources without a LayerNorm: those loads read zeros and touch no memory)
+        const rsrc_t rw = make_buf(a.lnw, a.lnw ? C * 4 : 0), rb = make_buf(a.lnb, a.lnb ? C * 4 : 0);
         float wv[8], bv[8];
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
@@ -98,6 +99,13 @@ __global__ __launch_bounds__(64 * kPjWaves) void ln_proj_kernel(PjArgs a) {
         const rsrc_t rm = make_buf(stats ? a.mean + row0 : nullptr, stats ? (uint32_t)nrows * 4u : 0u);
         const rsrc_t rr = make_buf(stats ? a.rstd + row0 : nullptr, stats ? (uint32_t)nrows * 4u : 0u);
         constexpr float inv_c = 1.0f / (float)C;
+        if (a.lnw == nullptr) {  // plain linear layer: the tile goes to LDS as it is
+#pragma unroll
+            for (int s = 0; s < G::SLOTS; ++s) {
+                const int r = wave * (G::TM / kPjWaves) + s * G::RPW + rs;
+                *(u32x4 *)(lds + r * G::STRIDE + li * 16) = raw[s];
+            }
+        } else {
 #pragma unroll
         for (int s = 0; s < G::SLOTS; ++s) {
             const int r = wave * (G::TM / kPjWaves) + s * G::RPW + rs;
@@ -129,6 +137,7 @@ __global__ __launch_bounds__(64 * kPjWaves) void ln_proj_kernel(PjArgs a) {
             const uint32_t so = li == 0 ? (uint32_t)r * 4u : kOOB;
             bstore4(__float_as_uint(k0 + mus), rm, so);
             bstore4(__float_as_uint(rstd), rr, so);
+        }
         }
     }
     __syncthreads();

@@ -126,6 +126,75 @@ int evo_ln_proj_bwd(const evo_proj_dims *d, const void *x, const float *ln_weigh
     return evo::launch_ln_proj_bwd(a, workspace, plan, (hipStream_t)stream) == hipSuccess ? EVO_OK : EVO_ERR_HIP;
 }
 
+int evo_linear_fwd(const evo_proj_dims *d, const void *x, const void *weight, const float *bias, void *const *outs,
+                   void *stream) {
+    const int st = check_proj(d);
+    if (st) return st;
+    if (d->n_rows == 0) return EVO_OK;
+    if (!x || !weight || !outs) return EVO_ERR_INVALID_ARG;
+    for (int p = 0; p < d->n_proj; ++p) {
+        if (!outs[p] || outs[p] == x || outs[p] == weight) return EVO_ERR_INVALID_ARG;
+        for (int q = 0; q < p; ++q)
+            if (outs[q] == outs[p]) return EVO_ERR_INVALID_ARG;
+        if (!aligned(outs[p], 16)) return EVO_ERR_ALIGNMENT;
+    }
+    if (!aligned(x, 16) || !aligned(weight, 16) || (bias && !aligned(bias, 16))) return EVO_ERR_ALIGNMENT;
+    evo::PjArgs a{};
+    a.x = x;
+    a.W = weight;
+    a.bias = bias;
+    a.out0 = outs[0];
+    a.out1 = d->n_proj > 1 ? outs[1] : nullptr;
+    a.out2 = d->n_proj > 2 ? outs[2] : nullptr;
+    a.out3 = d->n_proj > 3 ? outs[3] : nullptr;
+    a.R = d->n_rows;
+    a.C = d->c_in;
+    a.HD = d->proj_dim;
+    a.P = d->n_proj;
+    a.eps = d->eps;
+    return evo::launch_ln_proj(a, (hipStream_t)stream) == hipSuccess ? EVO_OK : EVO_ERR_HIP;
+}
+
+size_t evo_linear_bwd_workspace_size(const evo_proj_dims *d) {
+    if (check_proj(d)) return 0;
+    return evo::plan_proj_bwd(d->n_rows, d->c_in, d->proj_dim, d->n_proj, false).total;
+}
+
+int evo_linear_bwd(const evo_proj_dims *d, const void *x, const void *weight, const void *const *douts, void *dx,
+                   float *dweight, float *dbias, void *workspace, size_t workspace_bytes, void *stream) {
+    const int st = check_proj(d);
+    if (st) return st;
+    if (d->n_rows == 0) return EVO_OK;
+    if (!x || !weight || !douts || !dx || !dweight) return EVO_ERR_INVALID_ARG;
+    for (int p = 0; p < d->n_proj; ++p) {
+        if (!douts[p]) return EVO_ERR_INVALID_ARG;
+        if (!aligned(douts[p], 16)) return EVO_ERR_ALIGNMENT;
+    }
+    if (dx == x || (void *)dweight == (void *)dbias) return EVO_ERR_INVALID_ARG;
+    const void *al16[] = {x, weight, dx, dweight};
+    for (const void *q : al16)
+        if (!aligned(q, 16)) return EVO_ERR_ALIGNMENT;
+    if (dbias && !aligned(dbias, 16)) return EVO_ERR_ALIGNMENT;
+    const evo::PjBwdPlan plan = evo::plan_proj_bwd(d->n_rows, d->c_in, d->proj_dim, d->n_proj, false);
+    if (!workspace || workspace_bytes < plan.total || !aligned(workspace, 256)) return EVO_ERR_WORKSPACE;
+    evo::PjBwdArgs a{};
+    a.x = x;
+    a.y = x;
+    a.W = weight;
+    a.dout0 = douts[0];
+    a.dout1 = d->n_proj > 1 ? douts[1] : nullptr;
+    a.dout2 = d->n_proj > 2 ? douts[2] : nullptr;
+    a.dout3 = d->n_proj > 3 ? douts[3] : nullptr;
+    a.dx = dx;
+    a.dW = dweight;
+    a.dbias = dbias;
+    a.R = d->n_rows;
+    a.C = d->c_in;
+    a.HD = d->proj_dim;
+    a.P = d->n_proj;
+    return evo::launch_ln_proj_bwd(a, workspace, plan, (hipStream_t)stream) == hipSuccess ? EVO_OK : EVO_ERR_HIP;
+}
+
 // dims shared by the pair-bias forward and backward; `bwd` also requires the
 // backward's compiled head counts and its fp32 gradient plane below 2^31 bytes
 static int check_pb(const evo_pair_bias_dims *d, bool bwd) {

@@ -469,7 +469,9 @@ void launch_dw(dim3 grid, hipStream_t s, const PjBwdArgs &a, int64_t ct, int nfb
 template <int C>
 hipError_t launch_c(const PjBwdArgs &a, void *ws, const PjBwdPlan &plan, hipStream_t s) {
     char *w = (char *)ws;
-    void *dy = w + plan.off_dy;
+    // without a LayerNorm (a plain linear layer) dY is the input gradient itself
+    const bool ln = a.lnw != nullptr;
+    void *dy = ln ? w + plan.off_dy : a.dx;
     const int64_t nt = (a.R + 127) / 128;
     // split the channels when the token blocks alone leave CUs idle
     int ncs = 1;
@@ -485,11 +487,12 @@ hipError_t launch_c(const PjBwdArgs &a, void *ws, const PjBwdPlan &plan, hipStre
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    // LayerNorm backward of dY (bf16) -> dx, dln_w, dln_b
-    LnProblem lp{1, C, a.R, 0.0f};
-    LnBwdPtrs lx{a.x, a.lnw, a.mean, a.rstd, dy, a.dx, a.dlnw, a.dlnb};
-    e = launch_ln_bwd(lp, lx, w + plan.off_ln, s);
-    if (e != hipSuccess) return e;
+    if (ln) {  // LayerNorm backward of dY (bf16) -> dx, dln_w, dln_b
+        LnProblem lp{1, C, a.R, 0.0f};
+        LnBwdPtrs lx{a.x, a.lnw, a.mean, a.rstd, dy, a.dx, a.dlnw, a.dlnb};
+        e = launch_ln_bwd(lp, lx, w + plan.off_ln, s);
+        if (e != hipSuccess) return e;
+    }
     const int F = a.P * a.HD;
     float *pw = (float *)(w + plan.off_dw);
     float *pb = a.dbias ? (float *)(w + plan.off_db) : nullptr;
@@ -526,7 +529,7 @@ hipError_t launch_c(const PjBwdArgs &a, void *ws, const PjBwdPlan &plan, hipStre
 
 }  // namespace
 
-PjBwdPlan plan_proj_bwd(int64_t R, int C, int HD, int P) {
+PjBwdPlan plan_proj_bwd(int64_t R, int C, int HD, int P, bool ln) {
     PjBwdPlan pl{};
     const int F = P * HD;
     const int FB = proj_bwd_fb(C, HD, P);
@@ -550,9 +553,9 @@ PjBwdPlan plan_proj_bwd(int64_t R, int C, int HD, int P) {
     LnProblem lp{1, C, R, 0.0f};
     size_t off = 0;
     pl.off_dy = off;
-    off += align256((size_t)R * C * 2);
+    if (ln) off += align256((size_t)R * C * 2);
     pl.off_ln = off;
-    off += align256(ln_bwd_workspace(lp));
+    if (ln) off += align256(ln_bwd_workspace(lp));
     pl.off_dw = off;
     off += align256((size_t)pl.n_chunks * F * C * 4);
     pl.off_db = off;

@@ -44,6 +44,13 @@ def _lib():
         lib.evo_ln_proj_bwd.argtypes = [ctypes.POINTER(evo_proj_dims), P, P, P, P, P, P, ctypes.POINTER(P), P, P, P,
                                         P, P, P, ctypes.c_size_t, P]
         lib.evo_ln_proj_bwd.restype = ctypes.c_int
+        lib.evo_linear_fwd.argtypes = [ctypes.POINTER(evo_proj_dims), P, P, P, ctypes.POINTER(P), P]
+        lib.evo_linear_fwd.restype = ctypes.c_int
+        lib.evo_linear_bwd_workspace_size.argtypes = [ctypes.POINTER(evo_proj_dims)]
+        lib.evo_linear_bwd_workspace_size.restype = ctypes.c_size_t
+        lib.evo_linear_bwd.argtypes = [ctypes.POINTER(evo_proj_dims), P, P, ctypes.POINTER(P), P, P, P, P,
+                                       ctypes.c_size_t, P]
+        lib.evo_linear_bwd.restype = ctypes.c_int
         _bound = True
     return lib
 
@@ -124,6 +131,65 @@ def ln_proj_bwd(x, ln_weight, mean, rstd, y_norm, weight, douts, *, eps: float =
     if st:
         raise EvoAttnError(st, "evo_ln_proj_bwd")
     return dx, dweight, (dbias if has_bias else None), dln_weight, dln_bias
+
+
+def linear_fwd(x: torch.Tensor, weight: torch.Tensor, bias: Optional[torch.Tensor] = None, n_proj: int = 1, *,
+               outs: Optional[List[torch.Tensor]] = None, stream=None) -> List[torch.Tensor]:
+    """outs[p] = x @ weight[p*HD:(p+1)*HD].T + bias[p*HD:(p+1)*HD] (no LayerNorm),
+    e.g. the attention module's output projection."""
+    lib = _lib()
+    if x.dtype != torch.bfloat16 or weight.dtype != torch.bfloat16:
+        raise ValueError("x and weight must be bfloat16")
+    if not x.is_contiguous() or not weight.is_contiguous() or weight.dim() != 2:
+        raise ValueError("x and weight must be contiguous; weight is [n_proj*HD, C]")
+    C = x.shape[-1]
+    if weight.shape[1] != C or weight.shape[0] % n_proj:
+        raise ValueError("weight must be [n_proj*HD, C]")
+    HD = weight.shape[0] // n_proj
+    R = x.numel() // C if C else 0
+    if outs is None:
+        outs = [torch.empty(x.shape[:-1] + (HD,), dtype=torch.bfloat16, device=x.device) for _ in range(n_proj)]
+    if len(outs) != n_proj or any(o.dtype != torch.bfloat16 or not o.is_contiguous() or o.numel() != R * HD
+                                  for o in outs):
+        raise ValueError("outs must be n_proj contiguous bf16 tensors of R*HD elements")
+    d = evo_proj_dims(EVO_DTYPE_BF16, C, n_proj, HD, R, 0.0, 0)
+    ptrs = (ctypes.c_void_p * n_proj)(*[ctypes.c_void_p(o.data_ptr()) for o in outs])
+    st = lib.evo_linear_fwd(ctypes.byref(d), _ptr(x), _ptr(weight), _ptr(bias), ptrs, _stream(stream))
+    if st:
+        raise EvoAttnError(st, "evo_linear_fwd")
+    return outs
+
+
+def linear_bwd(x, weight, douts, *, has_bias: bool = True, dx=None, dweight=None, dbias=None, workspace=None,
+               stream=None):
+    """Gradients (dx, dweight, dbias or None) of linear_fwd for upstream
+    gradients douts (one [..., HD] bf16 tensor per projection)."""
+    lib = _lib()
+    P = len(douts)
+    C = x.shape[-1]
+    HD = weight.shape[0] // P
+    R = x.numel() // C if C else 0
+    for t in list(douts) + [x, weight]:
+        if t.dtype != torch.bfloat16 or not t.is_contiguous():
+            raise ValueError("x, weight and douts must be contiguous bfloat16")
+    if any(t.numel() != R * HD for t in douts):
+        raise ValueError("douts must hold R*HD elements")
+    dev = x.device
+    dx = torch.empty_like(x) if dx is None else dx
+    dweight = torch.empty((P * HD, C), dtype=torch.float32, device=dev) if dweight is None else dweight
+    if has_bias and dbias is None:
+        dbias = torch.empty(P * HD, dtype=torch.float32, device=dev)
+    d = evo_proj_dims(EVO_DTYPE_BF16, C, P, HD, R, 0.0, 0)
+    need = int(lib.evo_linear_bwd_workspace_size(ctypes.byref(d)))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    ptrs = (ctypes.c_void_p * P)(*[ctypes.c_void_p(t.data_ptr()) for t in douts])
+    st = lib.evo_linear_bwd(ctypes.byref(d), _ptr(x), _ptr(weight), ptrs, _ptr(dx), _ptr(dweight),
+                            _ptr(dbias if has_bias else None), _ptr(workspace),
+                            ctypes.c_size_t(workspace.numel() * workspace.element_size()), _stream(stream))
+    if st:
+        raise EvoAttnError(st, "evo_linear_bwd")
+    return dx, dweight, (dbias if has_bias else None)
 
 
 class evo_pair_bias_dims(ctypes.Structure):

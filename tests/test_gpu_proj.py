@@ -209,3 +209,58 @@ def test_backward_repeatable():
     torch.cuda.synchronize()
     for u, v in zip(a, b):
         assert torch.equal(u, v)
+
+
+# ---- linear layers without the LayerNorm (the output projection) -------------
+# Tolerances: forward as the LayerNorm variant (bf16 inputs are exact, the
+# output is rounded once); dx is dY rounded to bf16 once: |err| <= 2^-8 |ref|
+# + 1e-3 max|ref| of its row, 5e-3 normwise; dweight and dbias are fp32 sums of
+# exact bf16 products: 1e-4 normwise, 1e-4 max|ref| + 1e-4 |ref| per element.
+
+LINEAR_CASES = [
+    # R, C, HD, P, bias  (the first three: the output projections of the MSA
+    # row, triangle and extra-MSA attention workloads: C = H * d -> c_out)
+    (32768, 256, 256, 1, True),
+    (65536, 128, 128, 1, True),
+    (262144, 64, 64, 1, True),
+    (77, 256, 64, 2, False),
+    (1000, 128, 96, 3, True),
+    (4100, 64, 32, 4, True),
+]
+
+
+@pytest.mark.parametrize("case", LINEAR_CASES, ids=lambda c: "R%d_C%d_HD%d_P%d_b%d" % c)
+def test_linear_forward_backward(case):
+    R, C, HD, P, bias = case
+    print("\n[case] linear", case, flush=True)
+    rng = np.random.default_rng(R + C + HD + P)
+    x_np = W._store(rng.standard_normal((R, C)), "bf16")
+    w_np = W._store(rng.standard_normal((P * HD, C)) / np.sqrt(C), "bf16")
+    b_np = rng.standard_normal(P * HD).astype(np.float32) if bias else None
+    x, Wt = to_device(x_np, "bf16"), to_device(w_np, "bf16")
+    b = torch.from_numpy(b_np).cuda() if bias else None
+    outs = pj.linear_fwd(x, Wt, b, n_proj=P)
+    douts_np = [W._store(rng.standard_normal((R, HD)), "bf16") for _ in range(P)]
+    douts = [to_device(a, "bf16") for a in douts_np]
+    dx, dW, db = pj.linear_bwd(x, Wt, douts, has_bias=bias)
+    torch.cuda.synchronize()
+    xf, wf = W.as_float64(x_np, "bf16"), W.as_float64(w_np, "bf16")
+    # the full-size cases are checked on a sample of 2048 rows (the oracle's
+    # cost grows with R; the rows cover every workgroup position and the tail)
+    rows = np.unique(np.concatenate([np.linspace(0, R - 1, 1024).astype(int),
+                                     rng.integers(0, R, 1024)])) if R > 8192 else np.arange(R)
+    ref = oracle.linear_forward(xf[rows], wf, b_np, n_proj=P)
+    for p in range(P):
+        _check("linear out%d" % p, to_f64(outs[p])[rows], ref[p])
+    dfs = [W.as_float64(a, "bf16") for a in douts_np]
+    rdx, rdW, rdb = oracle.linear_backward(xf, wf, dfs)
+    gdx = to_f64(dx)
+    err = np.abs(gdx[rows] - rdx[rows])
+    bound = 2.0 ** -8 * np.abs(rdx[rows]) + 1e-3 * np.abs(rdx[rows]).max(axis=1, keepdims=True)
+    assert (err <= bound + 1e-30).all(), ("dx", float((err - bound).max()))
+    assert np.linalg.norm(gdx - rdx) / np.linalg.norm(rdx) <= 5e-3
+    _check("linear dW", to_f64(dW), rdW, atol=1e-4 * np.abs(rdW).max(), rtol=1e-4, norm=1e-4)
+    if bias:
+        _check("linear db", to_f64(db), rdb, atol=1e-5 * np.abs(rdb).max(), rtol=1e-5, norm=1e-5)
+    else:
+        assert db is None

@@ -27,7 +27,8 @@ def test_exports_declared_symbol():
                        open(os.path.join(ROOT, "include", "evo_proj.h")).read(), flags=re.M)
     assert set(decls) == {"evo_ln_proj_fwd", "evo_ln_proj_fwd_ex", "evo_ln_proj_bwd_workspace_size",
                           "evo_ln_proj_bwd", "evo_ln_pair_bias_fwd", "evo_ln_pair_bias_bwd_workspace_size",
-                          "evo_ln_pair_bias_bwd"}
+                          "evo_ln_pair_bias_bwd", "evo_linear_fwd", "evo_linear_bwd_workspace_size",
+                          "evo_linear_bwd"}
     for name in decls:
         assert hasattr(lib, name), name
 
@@ -110,3 +111,39 @@ def test_backward_rejects_bad_calls():
     assert _bwd(d, ws=None) == 4
     assert _bwd(_dims(n_rows=0), x=None, y=None, w=None, douts=None, dx=None) == 0
     assert lib.evo_ln_proj_bwd_workspace_size(ctypes.byref(_dims(c_in=96))) == 0
+
+
+
+# ---- linear layers (no LayerNorm) ---------------------------------------------
+
+def _lin_fwd(dims, x=FAKE, w=FAKE + 0x20000, b=None, outs=(FAKE + 0x100000,)):
+    arr = None if outs is None else (ctypes.c_void_p * len(outs))(*[ctypes.c_void_p(o) if o else None for o in outs])
+    return _lib().evo_linear_fwd(ctypes.byref(dims) if dims is not None else None, P(x), P(w), P(b), arr, None)
+
+
+def _lin_bwd(dims, x=FAKE, w=FAKE + 0x20000, douts=(FAKE + 0x100000,), dx=FAKE + 0x500000, dw=FAKE + 0x600000,
+             db=None, ws=FAKE + 0x1000000, ws_bytes=1 << 30):
+    arr = None if douts is None else (ctypes.c_void_p * len(douts))(*[ctypes.c_void_p(o) if o else None
+                                                                      for o in douts])
+    return _lib().evo_linear_bwd(ctypes.byref(dims) if dims is not None else None, P(x), P(w), arr, P(dx), P(dw),
+                                 P(db), P(ws), ctypes.c_size_t(ws_bytes), None)
+
+
+def test_linear_validation():
+    d = pj.evo_proj_dims(1, 256, 1, 256, 4096, 0.0, 0)
+    assert _lin_fwd(None) == 1
+    assert _lin_fwd(pj.evo_proj_dims(0, 256, 1, 256, 4096, 0.0, 0)) == 2
+    assert _lin_fwd(pj.evo_proj_dims(1, 96, 1, 256, 4096, 0.0, 0)) == 2
+    assert _lin_fwd(d, x=None) == 1 and _lin_fwd(d, w=None) == 1 and _lin_fwd(d, outs=None) == 1
+    assert _lin_fwd(d, outs=(FAKE,)) == 1                    # output aliases x
+    assert _lin_fwd(d, x=FAKE + 8) == 3 and _lin_fwd(d, outs=(FAKE + 0x100004,)) == 3
+    assert _lin_fwd(pj.evo_proj_dims(1, 256, 1, 256, 0, 0.0, 0), x=None, w=None, outs=None) == 0
+    need = _lib().evo_linear_bwd_workspace_size(ctypes.byref(d))
+    # no LayerNorm: only the weight-gradient partial sums
+    assert 0 < need < _lib().evo_ln_proj_bwd_workspace_size(ctypes.byref(d))
+    assert _lin_bwd(d, dx=None) == 1 and _lin_bwd(d, douts=(0,)) == 1
+    assert _lin_bwd(d, dx=FAKE) == 1                         # dx aliases x
+    assert _lin_bwd(d, ws_bytes=need - 1) == 4 and _lin_bwd(d, ws=FAKE + 0x1000010) == 4
+    assert _lin_bwd(d, douts=(FAKE + 0x100002,)) == 3
+    assert _lin_bwd(pj.evo_proj_dims(1, 256, 1, 256, 0, 0.0, 0), x=None, w=None, douts=None, dx=None, dw=None,
+                    ws=None, ws_bytes=0) == 0

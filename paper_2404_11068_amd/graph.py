@@ -100,8 +100,9 @@ class GraphCache:
 
 class MSARowAttentionStep:
     """Static buffers and weights of one MSA row attention with pair bias:
-    m [N, L, c_m], z [L, L, c_z] -> q, k, v, g, bias -> o, lse -> dq, dk, dv, dg, dbias -> dm and the
-    projection weight gradients, dz and the pair-bias weight gradients."""
+    m [N, L, c_m], z [L, L, c_z] -> q, k, v, g, bias -> o, lse -> m_out = o W_out^T + b_out; backward
+    from d_m_out: dout (at o), dW_out, db_out -> dq, dk, dv, dg, dbias -> dm and the projection weight
+    gradients, dz and the pair-bias weight gradients."""
 
     def __init__(self, N: int, L: int, c_m: int = 256, c_z: int = 128, H: int = 8, d: int = 32, seed: int = 0,
                  device="cuda"):
@@ -118,7 +119,14 @@ class MSARowAttentionStep:
         self.b_qkvg = torch.cat([torch.zeros(3 * H * d), torch.ones(H * d)]).to(**f32)  # gate bias 1
         self.w_bias = r(H, c_z, scale=c_z ** -0.5).to(**bf)
         self.mask = torch.ones(N, L, dtype=torch.uint8, device=device)
-        self.dout = r(N, L, H, d).to(**bf)
+        # output projection of the gated attention back to c_m, and the module's upstream gradient
+        self.w_out = r(c_m, H * d, scale=(H * d) ** -0.5).to(**bf)
+        self.b_out = (0.1 * r(c_m)).to(**f32)
+        self.m_out = torch.empty(N, L, c_m, **bf)
+        self.d_m_out = r(N, L, c_m).to(**bf)
+        self.dout = torch.empty(N, L, H, d, **bf)  # gradient at the attention output (from the projection)
+        self.dw_out = torch.empty(c_m, H * d, **f32)
+        self.db_out = torch.empty(c_m, **f32)
         self.q, self.k, self.v, self.gate = (torch.empty(N, L, H, d, **bf) for _ in range(4))
         self.bias = torch.empty(1, H, L, L, **bf)
         self.out = torch.empty(N, L, H, d, **bf)
@@ -138,6 +146,9 @@ class MSARowAttentionStep:
         dims = pj.evo_proj_dims(1, c_m, 4, H * d, N * L, 1e-5, 0)
         self.ws_proj = torch.empty(max(int(pj._lib().evo_ln_proj_bwd_workspace_size(ctypes.byref(dims))), 1),
                                    dtype=torch.uint8, device=device)
+        dims_o = pj.evo_proj_dims(1, H * d, 1, c_m, N * L, 0.0, 0)
+        self.ws_out = torch.empty(max(int(pj._lib().evo_linear_bwd_workspace_size(ctypes.byref(dims_o))), 1),
+                                  dtype=torch.uint8, device=device)
         # pair-bias gradients (the attention's dbias through LN(z) and the projection to heads)
         self.dz = torch.empty_like(self.z)
         self.dw_bias = torch.empty(H, c_z, **f32)
@@ -154,13 +165,20 @@ class MSARowAttentionStep:
         return self._key
 
     def record(self, stream):
-        """Enqueue the step (6 C-ABI calls, 16 kernels) on `stream` (torch stream or raw handle)."""
+        """Enqueue the step (8 C-ABI calls, 18 kernels) on `stream` (torch stream or raw handle):
+        projections, pair bias, attention, output projection; then the backward in reverse."""
         pj.ln_proj_fwd(self.m, self.ln_m_w, self.ln_m_b, self.w_qkvg, self.b_qkvg, n_proj=4,
                        outs=[t.view(self.N, self.L, -1) for t in (self.q, self.k, self.v, self.gate)],
                        mean=self.mean, rstd=self.rstd, y_norm=self.y_norm, stream=stream)
         pj.ln_pair_bias_fwd(self.z, self.ln_z_w, self.ln_z_b, self.w_bias, out=self.bias, stream=stream)
         ea.evo_attn_fwd(self.q, self.k, self.v, self.gate, self.bias, self.mask, rows_per_bias=self.N,
                         out=self.out, lse=self.lse, stream=stream)
+        HDm = self.H * self.d
+        pj.linear_fwd(self.out.view(self.N, self.L, HDm), self.w_out, self.b_out,
+                      outs=[self.m_out], stream=stream)
+        pj.linear_bwd(self.out.view(self.N, self.L, HDm), self.w_out, [self.d_m_out],
+                      dx=self.dout.view(self.N, self.L, HDm), dweight=self.dw_out, dbias=self.db_out,
+                      workspace=self.ws_out, stream=stream)
         ea.evo_attn_bwd(self.q, self.k, self.v, self.gate, self.bias, self.mask, self.out, self.lse, self.dout,
                         rows_per_bias=self.N, dq=self.dq, dk=self.dk, dv=self.dv, dgate=self.dg, dbias=self.dbias,
                         workspace=self.ws, stream=stream)
@@ -175,4 +193,5 @@ class MSARowAttentionStep:
     def outputs(self):
         return {k: getattr(self, k) for k in ("q", "k", "v", "gate", "bias", "out", "lse", "dq", "dk", "dv", "dg",
                                                "dbias", "y_norm", "dm", "dw_qkvg", "db_qkvg", "dln_m_w", "dln_m_b",
-                                               "dz", "dw_bias", "dln_z_w", "dln_z_b")}
+                                               "dz", "dw_bias", "dln_z_w", "dln_z_b", "m_out", "dout", "dw_out",
+                                               "db_out")}

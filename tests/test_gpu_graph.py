@@ -1,6 +1,6 @@
 """GPU checks of the HIP graph cache on an MSA-row-attention step
-(LayerNorm + projections, pair bias, attention forward and backward, and the
-backward of the projections and of the pair bias).
+(LayerNorm + projections, pair bias, attention, output projection, and the
+backward of all of them).
 
 * a replayed graph gives bitwise the results of the same step run eagerly
   (every kernel is deterministic), over several replays with new input
@@ -31,7 +31,7 @@ def test_replay_matches_eager_over_new_inputs():
         if it:
             step.m.copy_(torch.randn(step.m.shape, generator=gen).to(torch.bfloat16))
             step.z.copy_(torch.randn(step.z.shape, generator=gen).to(torch.bfloat16))
-            step.dout.copy_(torch.randn(step.dout.shape, generator=gen).to(torch.bfloat16))
+            step.d_m_out.copy_(torch.randn(step.d_m_out.shape, generator=gen).to(torch.bfloat16))
         torch.cuda.synchronize()
         with torch.cuda.stream(s):
             step.record(s)

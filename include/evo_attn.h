@@ -138,7 +138,10 @@ int evo_attn_bwd(const evo_attn_dims *dims, const void *q, const void *k, const 
  * events[0] on `stream` before its first kernel and events[i] right after its
  * i-th kernel, so event pairs bracket single kernels.  Kernel order in this
  * version: [pair-bias transpose], dK/dV pass, dQ/dBias pass, [dBias reduce]
- * (bracketed entries only when bias != NULL).  n_events must be at least
+ * (bracketed entries only when bias != NULL).  The transpose runs only for
+ * fp32 or a seq_len that is not a multiple of 8; otherwise the dK/dV pass reads
+ * the bias as it is and events[0] and events[1] bracket no kernel (the slot is
+ * kept so that the event count depends on has_bias alone).  n_events must be at least
  * evo_attn_bwd_kernel_count(bias != NULL) + 1 and every handle non-NULL,
  * else EVO_ERR_INVALID_ARG.  Meant for benchmarks; recording events costs a
  * few microseconds per call.

@@ -106,7 +106,9 @@ __global__ void __launch_bounds__(256) transpose_kernel(const E *__restrict__ sr
 
 // ---------------------------------------------------------------------------
 struct KvArgs {
-    const void *q, *k, *v, *g, *out, *dout, *biasT;
+    const void *q, *k, *v, *g, *out, *dout;
+    const void *bias;   // [planes][H][L][L], read directly (bf16, L % 8 == 0)
+    const void *biasT;  // its transpose in the workspace (other cases)
     const uint8_t *mask;
     const float *lse;
     void *dk, *dv, *dg;
@@ -116,6 +118,47 @@ struct KvArgs {
     int H;
     float scale;
 };
+
+// bf16 pair bias of (query tile qt, key tile kt) as it lies in memory: lane
+// l holds the 16-byte chunks l and l + 64 of the 32 x 32 block (row = chunk
+// / 4 = query, 8 keys per chunk).  Rows past L read zeros.
+__device__ __forceinline__ void bias_block_load(rsrc_t rb, int L, int qt, int kt, int lane, u32x4 (&raw)[2]) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int r = (lane >> 2) + 16 * j, cc = lane & 3;
+        const int qi = qt * 32 + r;
+        raw[j] = bload16(rb, qi < L ? (uint32_t)(qi * L + kt * 32 + 8 * cc) * 2u : kOOB);
+    }
+}
+
+// The block through this wave's own 32 x 32 LDS tile (no barrier: a wave's
+// LDS accesses complete in order): stored with column c holding key sig(c),
+// then read back with the transposing read, which hands lane n the column
+// sig(n), i.e. key n, at the query rows krow(i, h) of register i -- the
+// logit layout of the kv tile.
+__device__ __forceinline__ void bias_block_transpose(uint16_t *tile, const u32x4 (&raw)[2], int lane,
+                                                     float *out16) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int r = (lane >> 2) + 16 * j, cc = lane & 3;
+        // keys 8cc + 4b + e (e < 4) go to column sig(8cc + 4b + e) = 16(cc/2) + 8b + 4(cc%2) + e
+        const int c0 = 16 * (cc >> 1) + 4 * (cc & 1);
+        const u32x2 lo = {raw[j].x, raw[j].y}, hi = {raw[j].z, raw[j].w};
+        *reinterpret_cast<u32x2 *>(&tile[r * 32 + c0]) = lo;
+        *reinterpret_cast<u32x2 *>(&tile[r * 32 + c0 + 8]) = hi;
+    }
+    const Tr<bf16_t>::K32 f = load_k32_tr(tile, 32, 0, 32, lane);
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+        const u32x4 w = __builtin_bit_cast(u32x4, f.v[t]);
+        const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int s2 = 0; s2 < 4; ++s2) {
+            out16[8 * t + 2 * s2] = __builtin_bit_cast(float, ws[s2] << 16);
+            out16[8 * t + 2 * s2 + 1] = __builtin_bit_cast(float, ws[s2] & 0xffff0000u);
+        }
+    }
+}
 
 template <typename T, int D, int NKT, bool BV>
 __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
@@ -132,12 +175,16 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
     // bf16: Q^T and dA^T fragments come from the transposing LDS read of the
     // row-major tiles; fp32 keeps explicit transposed copies
     constexpr bool kTr = ES == 2;
+    // bf16 with whole 16-byte bias row groups: the bias is read as it lies in
+    // memory and transposed per tile in LDS; otherwise from its transpose
+    constexpr bool kBD = kTr && BV;
     __shared__ __attribute__((aligned(16))) E q_lds[LP * RSTR];
     __shared__ __attribute__((aligned(16))) E da_lds[LP * RSTR];
     __shared__ __attribute__((aligned(16))) E qt_lds[kTr ? 8 : D * TSTR];
     __shared__ __attribute__((aligned(16))) E dat_lds[kTr ? 8 : D * TSTR];
     __shared__ __attribute__((aligned(16))) float lse2_lds[LP];
     __shared__ __attribute__((aligned(16))) float dsum_lds[LP];
+    __shared__ __attribute__((aligned(16))) uint16_t bt_lds[kBD ? NKT * 32 * 32 : 8];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int h2 = lane >> 5, n = lane & 31;
@@ -148,7 +195,8 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
     const int64_t r = unit / a.H;
     const int64_t b = r / a.rpb;
     const int64_t rh = r * a.H + hh;
-    const bool has_gate = a.g != nullptr, has_mask = a.mask != nullptr, has_bias = a.biasT != nullptr;
+    const bool has_gate = a.g != nullptr, has_mask = a.mask != nullptr,
+               has_bias = (kBD ? a.bias : a.biasT) != nullptr;
     const uint32_t stok_b = (uint32_t)(a.stok * ES);
     const uint32_t row_bytes = (uint32_t)(a.L * a.stok * ES);
     const rsrc_t none = make_buf(nullptr, 0u);
@@ -181,12 +229,15 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
             gv[j] = bload16(rg, off);
         }
     }
-    // bias^T rows of this lane's key: reg i <-> query qt*32 + krow(i, h2)
-    const rsrc_t rbt = has_bias ? make_buf((const E *)a.biasT + (b * a.H + hh) * (int64_t)L * L, (uint32_t)(L * L * ES))
+    // bias of this lane's key: reg i <-> query qt*32 + krow(i, h2)
+    const rsrc_t rbt = has_bias ? make_buf((const E *)(kBD ? a.bias : a.biasT) + (b * a.H + hh) * (int64_t)L * L,
+                                           (uint32_t)(L * L * ES))
                                 : none;
     const uint32_t bt_e0 = (uint32_t)key * (uint32_t)L + 8u * h2;  // element of query 8*h2 in this key's row
     float bcur[16];
-    load_bias16<T, BV>(rbt, bt_e0, bcur);
+    u32x4 braw[2];  // kBD: raw block of the next query tile
+    if constexpr (kBD) bias_block_load(rbt, L, 0, kt, lane, braw);
+    else load_bias16<T, BV>(rbt, bt_e0, bcur);
 
     // ---- stage Q and dA (both layouts); dA, Dsum and dG come from dO, O, G
     {
@@ -243,6 +294,8 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
     const float keepf = kvalid ? 1.0f : 0.0f;  // masked key: its lane's P is 0
     const float c2 = a.scale * kLog2e;
     const int arow = sig(n);  // permuted A-operand row of this lane
+    uint16_t *const bt_tile = &bt_lds[kBD ? wave * 1024 : 0];
+    if constexpr (kBD) bias_block_transpose(bt_tile, braw, lane, bcur);
     __syncthreads();
 
     f32x16 dv_acc = zero16(), dk_acc = zero16();
@@ -251,8 +304,11 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
     for (int qt = 0; qt < NKT; ++qt) {
         if (qt >= nqt) break;
         // the next tile's bias goes out first (loads complete in order)
-        float bnext[16];
-        if (qt + 1 < NKT) load_bias16<T, BV>(rbt, bt_e0 + 32u * (qt + 1), bnext);
+        float bnext[kBD ? 1 : 16];
+        if (qt + 1 < NKT) {
+            if constexpr (kBD) bias_block_load(rbt, L, qt + 1, kt, lane, braw);
+            else load_bias16<T, BV>(rbt, bt_e0 + 32u * (qt + 1), bnext);
+        }
         // S = Q K^T and dP = dA V^T for 32 queries x this wave's 32 keys;
         // lane = key, reg i = query qt*32 + krow(i, h2)
         ChFrag<T, D> qa, daa;
@@ -297,8 +353,12 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
         Tr<T>::mma_k32(dv_acc, dat, pb);
         Tr<T>::mma_k32(dk_acc, qtf, dsb);
         if (qt + 1 < NKT) {
+            if constexpr (kBD) {
+                bias_block_transpose(bt_tile, braw, lane, bcur);
+            } else {
 #pragma unroll
-            for (int i = 0; i < 16; ++i) bcur[i] = bnext[i];
+                for (int i = 0; i < 16; ++i) bcur[i] = bnext[i];
+            }
         }
     }
 
@@ -645,6 +705,9 @@ __global__ void __launch_bounds__(256) dbias_reduce_kernel(const float *__restri
 // ---------------------------------------------------------------------------
 inline unsigned round8(int64_t n) { return (unsigned)((n + 7) / 8 * 8); }
 
+// bf16 bias rows made of whole 16-byte groups: kv reads the bias as it is
+inline bool bias_direct(const Problem &p) { return p.dtype == 1 && p.L % 8 == 0; }
+
 template <typename T, int D, int NKT, bool BV>
 hipError_t launch_passes(const Problem &p, const KvArgs &ka, const QbArgs &qa, hipStream_t s, Tracer &tr) {
     // grids are rounded up to a multiple of 8 for the XCD-aware unit order;
@@ -683,7 +746,11 @@ hipError_t launch_bwd_t(const Problem &p, const BwdPtrs &x, void *ws, const BwdP
     const int64_t planes = x.bias ? (p.N / p.rpb) * p.H : 0;
     hipError_t e;
     tr.mark(s);
-    if (x.bias) {
+    // the kv pass reads a bf16 bias with whole 16-byte row groups directly
+    // (the first traced interval is then empty)
+    const bool bias_t = x.bias && !bias_direct(p);
+    if (!bias_t && x.bias) tr.mark(s);
+    if (bias_t) {
         const int64_t tiles = (p.L + 31) / 32;
         hipLaunchKernelGGL((transpose_kernel<E>), dim3((unsigned)(planes * tiles * tiles)), dim3(256), 0, s,
                            (const E *)x.bias, (E *)(w + plan.off_biast), p.L, tiles);
@@ -695,7 +762,8 @@ hipError_t launch_bwd_t(const Problem &p, const BwdPtrs &x, void *ws, const BwdP
     const float scale = 1.0f / sqrtf((float)p.D);
     KvArgs ka;
     ka.q = x.q; ka.k = x.k; ka.v = x.v; ka.g = x.g; ka.out = x.out; ka.dout = x.dout;
-    ka.biasT = x.bias ? (const void *)(w + plan.off_biast) : nullptr;
+    ka.bias = x.bias;
+    ka.biasT = bias_t ? (const void *)(w + plan.off_biast) : nullptr;
     ka.mask = x.mask; ka.lse = x.lse;
     ka.dk = x.dk; ka.dv = x.dv; ka.dg = x.dg;
     ka.da = w + plan.off_da; ka.dsum = (float *)(w + plan.off_dsum);
@@ -761,7 +829,7 @@ BwdPlan plan_bwd(const Problem &p, bool has_bias) {
     pl.off_dsum = off;
     off = align256(off + (size_t)(p.N * p.H * p.L) * 4);
     pl.off_biast = off;
-    if (has_bias) off = align256(off + (size_t)(planes * p.H * p.L * p.L * es));
+    if (has_bias && !bias_direct(p)) off = align256(off + (size_t)(planes * p.H * p.L * p.L * es));
     pl.off_part = off;
     if (has_bias) off = align256(off + (size_t)(planes * p.H * chunks * p.L * p.L) * 4);
     pl.total = off;

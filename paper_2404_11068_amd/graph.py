@@ -165,7 +165,7 @@ class MSARowAttentionStep:
         return self._key
 
     def record(self, stream):
-        """Enqueue the step (8 C-ABI calls, 18 kernels) on `stream` (torch stream or raw handle):
+        """Enqueue the step (8 C-ABI calls, 17 kernels) on `stream` (torch stream or raw handle):
         projections, pair bias, attention, output projection; then the backward in reverse."""
         pj.ln_proj_fwd(self.m, self.ln_m_w, self.ln_m_b, self.w_qkvg, self.b_qkvg, n_proj=4,
                        outs=[t.view(self.N, self.L, -1) for t in (self.q, self.k, self.v, self.gate)],

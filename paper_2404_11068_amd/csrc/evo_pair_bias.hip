@@ -7,15 +7,18 @@
 // triangle attention around the ending node, bias[b, h, j, i]) directly, so
 // the [B, Li, Lj, H] intermediate and its transpose never reach HBM.
 //
-// Workgroup = 4 waves = 4 rows i of one batch entry times 32 columns j.  In a
+// Workgroup = 4 waves = 4 rows i of one batch entry times 16 columns j.  In a
 // wave, a pair entry of C channels is read by LPR = C / 8 lanes (16 bytes
 // each; all the wave's loads are issued before any arithmetic).  LayerNorm
 // statistics come from DPP row reductions; the normalised entry is rounded
 // to bf16 and each head's dot product is four v_dot2_f32_bf16 per lane; the
 // H partial sums are then reduce-scattered over the entry's lanes (each lane
-// ends with the full sum of one head, or of H/LPR heads).  The H x 4 x 32 results go through LDS so that the
-// stores cover 16 contiguous bytes (plain layout) or 8 (transposed).
-// Lengths are multiples of 8, so no 16- or 8-byte piece straddles a row.
+// ends with the full sum of one head, or of H/LPR heads).  The H x 4 x 16
+// results go through LDS so that the stores cover 16 contiguous bytes (plain
+// layout) or 8 (transposed).  Lengths are multiples of 8, so no 16- or 8-byte
+// piece straddles a row.  Sixteen columns per workgroup (not 32) give four
+// waves per SIMD at the 256 x 256 crop, which hides more of each wave's
+// single batch of loads (pair_bias_kernel<128, 8>: 9.3 -> 8.4 us mean).
 #include "evo_frag.h"
 #include "evo_kernels.h"
 
@@ -23,7 +26,7 @@ namespace evo {
 namespace {
 
 constexpr int kPbWaves = 4;  // rows i per workgroup, one per wave
-constexpr int kPbTJ = 32;    // columns j per workgroup
+constexpr int kPbTJ = 16;    // columns j per workgroup
 
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
 
@@ -195,9 +198,10 @@ __global__ __launch_bounds__(64 * kPbWaves) void pair_bias_kernel(PbArgs a) {
 
     const rsrc_t ro = make_buf((char *)a.out + b * H * (int64_t)Li * Lj * 2, (uint32_t)(H * Li * Lj) * 2u);
     if (!a.transpose) {
-        // rows (h, i) of 32 columns: 4 pieces of 8 columns each
-        for (int idx = threadIdx.x; idx < H * kPbWaves * 4; idx += 64 * kPbWaves) {
-            const int h = idx / (kPbWaves * 4), w = (idx / 4) % kPbWaves, ch = idx % 4;
+        // rows (h, i) of kPbTJ columns: pieces of 8 columns
+        constexpr int NPC = kPbTJ / 8;
+        for (int idx = threadIdx.x; idx < H * kPbWaves * NPC; idx += 64 * kPbWaves) {
+            const int h = idx / (kPbWaves * NPC), w = (idx / NPC) % kPbWaves, ch = idx % NPC;
             const u32x4 v = *(const u32x4 *)&stage[h][w][ch * 8];
             const int ii = i0 + w, jj = j0 + ch * 8;
             const bool ok = ii < Li && jj < Lj;

@@ -161,3 +161,24 @@ def test_unsupported_shapes_raise():
     q = torch.zeros((2, 16, 2, 24), dtype=torch.bfloat16, device="cuda")
     with pytest.raises(ea.EvoAttnError):
         ea.evo_attn_fwd(q, q, q)
+
+
+@pytest.mark.parametrize("dtype,L", [("bf16", 96), ("bf16", 90), ("f32", 64)])
+def test_traced_backward_matches_plain(dtype, L):
+    """The profiling entry point gives the same bits as the plain backward, on
+    both bias paths (a bf16 bias of whole 16-byte rows is read directly; fp32
+    and other lengths go through the transpose kernel), and its events bracket
+    non-negative intervals."""
+    w, x = make_inputs(3, L, 2, 32, dtype, seed=31 + L)
+    print("\n[case] traced backward", dtype, L, flush=True)
+    dev = {n: to_device(x[n], dtype) for n in ("q", "k", "v", "gate", "bias", "dout")}
+    mask = torch.from_numpy(x["mask"]).cuda()
+    args = (dev["q"], dev["k"], dev["v"], dev["gate"], dev["bias"], mask)
+    out, lse = ea.evo_attn_fwd(*args, rows_per_bias=w.rows_per_bias)
+    plain = ea.evo_attn_bwd(*args, out, lse, dev["dout"], rows_per_bias=w.rows_per_bias)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(ea.evo_attn_bwd_kernel_count(True) + 1)]
+    traced = ea.evo_attn_bwd(*args, out, lse, dev["dout"], rows_per_bias=w.rows_per_bias, events=ev)
+    torch.cuda.synchronize()
+    for a, b in zip(plain, traced):
+        assert torch.equal(a, b)
+    assert all(ev[j].elapsed_time(ev[j + 1]) >= 0.0 for j in range(len(ev) - 1))

@@ -70,8 +70,14 @@ enum evo_attn_status {
     EVO_ERR_HIP = 5          /* a kernel launch failed (hipGetLastError after the launch) */
 };
 
-/* Compiled limits: head_dim in {8, 16, 32}; 0 <= seq_len <= EVO_ATTN_MAX_SEQ_LEN. */
+/* Compiled limits: head_dim in {8, 16, 32, 64}; 0 <= seq_len <= EVO_ATTN_MAX_SEQ_LEN
+ * (fp32 with head_dim 64: seq_len <= EVO_ATTN_MAX_SEQ_LEN_F32_D64, the most the
+ * backward's LDS tiles hold).  Head dims 8, 16 and 32 cover every Evoformer
+ * attention (MSA row and column, triangle, extra-MSA); head_dim 64 runs each
+ * (row, head) as two workgroups that form the same logits from all 64 channels
+ * and produce 32 output channels each. */
 #define EVO_ATTN_MAX_SEQ_LEN 256
+#define EVO_ATTN_MAX_SEQ_LEN_F32_D64 128
 
 typedef struct evo_attn_dims {
     int32_t dtype;         /* enum evo_attn_dtype */

@@ -19,8 +19,11 @@ int check_dims(const evo_attn_dims *d, bool has_bias, evo::Problem *p) {
     if (d->reserved != 0) return EVO_ERR_INVALID_ARG;
     if (d->dtype != EVO_DTYPE_F32 && d->dtype != EVO_DTYPE_BF16) return EVO_ERR_UNSUPPORTED;
     if (d->n_heads < 1 || d->head_dim < 1 || d->n_rows < 0 || d->seq_len < 0) return EVO_ERR_INVALID_ARG;
-    if (d->head_dim != 8 && d->head_dim != 16 && d->head_dim != 32) return EVO_ERR_UNSUPPORTED;
+    if (d->head_dim != 8 && d->head_dim != 16 && d->head_dim != 32 && d->head_dim != 64) return EVO_ERR_UNSUPPORTED;
     if (d->seq_len > EVO_ATTN_MAX_SEQ_LEN) return EVO_ERR_UNSUPPORTED;
+    // fp32 at head_dim 64: the backward's LDS tiles fit up to 128 keys
+    if (d->dtype == EVO_DTYPE_F32 && d->head_dim == 64 && d->seq_len > EVO_ATTN_MAX_SEQ_LEN_F32_D64)
+        return EVO_ERR_UNSUPPORTED;
     const int64_t hd = (int64_t)d->n_heads * d->head_dim;
     if (d->stride_tok < hd || d->stride_row < hd) return EVO_ERR_INVALID_ARG;
     // the (row, token) grid must not overlap itself: either rows are outermost
@@ -31,9 +34,10 @@ int check_dims(const evo_attn_dims *d, bool has_bias, evo::Problem *p) {
     if (has_bias) {
         if (d->rows_per_bias < 1 || d->n_rows % d->rows_per_bias != 0) return EVO_ERR_INVALID_ARG;
     }
-    // grid limits of the kernels
-    if ((int64_t)d->n_rows * d->n_heads > 0x7fffffffLL) return EVO_ERR_UNSUPPORTED;
-    if ((int64_t)d->n_rows * d->seq_len * d->n_heads / 256 > 0x7fffffffLL) return EVO_ERR_UNSUPPORTED;
+    // grid limits of the kernels (head_dim 64 takes two workgroups per unit)
+    const int64_t halves = d->head_dim > 32 ? 2 : 1;
+    if ((int64_t)d->n_rows * d->n_heads * halves > 0x7fffffffLL) return EVO_ERR_UNSUPPORTED;
+    if ((int64_t)d->n_rows * d->seq_len * d->n_heads * halves / 256 > 0x7fffffffLL) return EVO_ERR_UNSUPPORTED;
     const int es = d->dtype == EVO_DTYPE_BF16 ? 2 : 4;
     if ((d->stride_tok * es) % 16 != 0 || (d->stride_row * es) % 16 != 0) return EVO_ERR_ALIGNMENT;
     // the kernels address the tokens of one row with 32-bit byte offsets

@@ -172,6 +172,11 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
     constexpr int RSTR = D + VEC;    // row-major LDS stride
     constexpr int TSTR = LP + VEC;   // transposed LDS stride
     constexpr int NST = (LP * CPT + NT - 1) / NT;  // staged 16-byte chunks per thread
+    // output channels per workgroup: head_dim 64 runs as two units per (row,
+    // head), both forming S and dP from all 64 channels, each producing 32
+    // channels of dK and dV; the first also writes dA, dG and Dsum
+    constexpr int DO = D > 32 ? 32 : D;
+    constexpr int NHALF = D / DO;
     // bf16: Q^T and dA^T fragments come from the transposing LDS read of the
     // row-major tiles; fp32 keeps explicit transposed copies
     constexpr bool kTr = ES == 2;
@@ -180,8 +185,8 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
     constexpr bool kBD = kTr && BV;
     __shared__ __attribute__((aligned(16))) E q_lds[LP * RSTR];
     __shared__ __attribute__((aligned(16))) E da_lds[LP * RSTR];
-    __shared__ __attribute__((aligned(16))) E qt_lds[kTr ? 8 : D * TSTR];
-    __shared__ __attribute__((aligned(16))) E dat_lds[kTr ? 8 : D * TSTR];
+    __shared__ __attribute__((aligned(16))) E qt_lds[kTr ? 8 : DO * TSTR];
+    __shared__ __attribute__((aligned(16))) E dat_lds[kTr ? 8 : DO * TSTR];
     __shared__ __attribute__((aligned(16))) float lse2_lds[LP];
     __shared__ __attribute__((aligned(16))) float dsum_lds[LP];
     __shared__ __attribute__((aligned(16))) uint16_t bt_lds[kBD ? NKT * 32 * 32 : 8];
@@ -189,10 +194,13 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int h2 = lane >> 5, n = lane & 31;
     const int L = (int)a.L;
-    const int64_t unit = xcd_unit(blockIdx.x, gridDim.x);  // (row, head), head fastest
+    const int64_t unit = xcd_unit(blockIdx.x, gridDim.x);  // (row, head[, half]), head fastest
     if (unit >= a.n_units) return;
-    const int hh = (int)(unit % a.H);
-    const int64_t r = unit / a.H;
+    const int ch = NHALF == 1 ? 0 : (int)(unit % NHALF);
+    const int c_off = ch * DO;  // first output channel of the unit
+    const bool writer = ch == 0;  // writes the per-token outputs shared by the halves
+    const int hh = (int)(unit / NHALF % a.H);
+    const int64_t r = unit / NHALF / a.H;
     const int64_t b = r / a.rpb;
     const int64_t rh = r * a.H + hh;
     const bool has_gate = a.g != nullptr, has_mask = a.mask != nullptr,
@@ -268,20 +276,24 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
             // Dsum of the token: sum over its CPT consecutive lanes
 #pragma unroll
             for (int off = 1; off < CPT; off <<= 1) part += __shfl_xor(part, off);
-            const uint32_t toff = valid ? (uint32_t)t * stok_b + (uint32_t)(c * ES) : kOOB;
+            const bool wv = valid && writer;
+            const uint32_t toff = wv ? (uint32_t)t * stok_b + (uint32_t)(c * ES) : kOOB;
             bstore16(dgv, rdg, toff);  // dropped without a gate
-            bstore16(dav, rda, valid ? (uint32_t)((t * D + c) * ES) : kOOB);
-            bstore4(__builtin_bit_cast(uint32_t, part), rds, (valid && c == 0) ? (uint32_t)t * 4u : kOOB);
+            bstore16(dav, rda, wv ? (uint32_t)((t * D + c) * ES) : kOOB);
+            bstore4(__builtin_bit_cast(uint32_t, part), rds, (wv && c == 0) ? (uint32_t)t * 4u : kOOB);
             if (in) {
                 if (c == 0) dsum_lds[t] = valid ? part : 0.0f;
                 *reinterpret_cast<u32x4 *>(&q_lds[t * RSTR + c]) = qv[j];
                 *reinterpret_cast<u32x4 *>(&da_lds[t * RSTR + c]) = dav;
                 if constexpr (!kTr) {
                     const E *qe = reinterpret_cast<const E *>(&qv[j]);
+                    const int cq = c - c_off;  // transposed copies: the unit's channels only
+                    if (NHALF == 1 || (cq >= 0 && cq < DO)) {
 #pragma unroll
-                    for (int e = 0; e < VEC; ++e) {
-                        qt_lds[(c + e) * TSTR + t] = qe[e];
-                        dat_lds[(c + e) * TSTR + t] = dae[e];
+                        for (int e = 0; e < VEC; ++e) {
+                            qt_lds[(cq + e) * TSTR + t] = qe[e];
+                            dat_lds[(cq + e) * TSTR + t] = dae[e];
+                        }
                     }
                 }
             }
@@ -341,9 +353,9 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
         // dV^T += dA^T P ;  dK^T += Q^T dS   (A rows: channel sig(n))
         K32 dat, qtf;
         if constexpr (kTr) {
-            dat = load_k32_tr(da_lds, RSTR, qt * 32, D, lane);
-            qtf = load_k32_tr(q_lds, RSTR, qt * 32, D, lane);
-        } else if (arow < D) {
+            dat = load_k32_tr(da_lds + c_off, RSTR, qt * 32, DO, lane);
+            qtf = load_k32_tr(q_lds + c_off, RSTR, qt * 32, DO, lane);
+        } else if (arow < DO) {
             dat = load_k32<T>(&dat_lds[arow * TSTR + qt * 32], h2);
             qtf = load_k32<T>(&qt_lds[arow * TSTR + qt * 32], h2);
         } else {
@@ -367,8 +379,8 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
         const int c0 = 16 * half + 8 * h2;
-        if (16 * half >= D) continue;
-        const uint32_t off = c0 < D ? key_off + (uint32_t)(c0 * ES) : kOOB;
+        if (16 * half >= DO) continue;
+        const uint32_t off = c0 < DO ? key_off + (uint32_t)((c_off + c0) * ES) : kOOB;
         const int o = 8 * half;
         if constexpr (ES == 2) {
             u32x4 wk, wv;
@@ -436,7 +448,12 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(4
     constexpr int KSTR = kSw ? D : D + VEC;  // row stride of K, V, Q, dA tiles in LDS (elements)
     constexpr int NKV = (LP * CPT + NT - 1) / NT;  // 16-byte chunks of K (and of V) per thread
     constexpr int NQC = (32 * CPT + NT - 1) / NT;  // 16-byte chunks of the Q (and dA) tile per thread
-    constexpr int NSUM = (32 * (D / 4) + NT - 1) / NT;  // 4-channel groups of dQ summed per thread
+    // output channels per workgroup: head_dim 64 runs as two units per (row
+    // chunk, query tile, head), both forming S^T and dP^T from all 64 channels,
+    // each producing 32 channels of dQ; the first writes the dBias partial
+    constexpr int DO = D > 32 ? 32 : D;
+    constexpr int NHALF = D / DO;
+    constexpr int NSUM = (32 * (DO / 4) + NT - 1) / NT;  // 4-channel groups of dQ summed per thread
     __shared__ __attribute__((aligned(16))) E k_lds[LP * KSTR];
     __shared__ __attribute__((aligned(16))) E v_lds[LP * KSTR];
     __shared__ __attribute__((aligned(16))) E q_lds[32 * KSTR];
@@ -444,17 +461,19 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(4
     __shared__ __attribute__((aligned(16))) float lse2_lds[32];
     __shared__ __attribute__((aligned(16))) float dsum_lds[32];
     __shared__ uint32_t kbits_lds[NKT];
-    __shared__ __attribute__((aligned(16))) float dqp[NKT * 32 * D];
+    __shared__ __attribute__((aligned(16))) float dqp[NKT * 32 * DO];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int h2 = lane >> 5, n = lane & 31;
     const int L = (int)a.L;
     const int nqt = (L + 31) / 32;
-    // unit -> (b, chunk, qt, head), head fastest
+    // unit -> (b, chunk, qt, head[, half]), head fastest
     const int64_t unit = xcd_unit(blockIdx.x, gridDim.x);
     if (unit >= a.n_units) return;
-    const int hh = (int)(unit % a.H);
-    int64_t rest = unit / a.H;
+    const int ch = NHALF == 1 ? 0 : (int)(unit % NHALF);
+    const int c_off = ch * DO;  // first output channel of the unit
+    const int hh = (int)(unit / NHALF % a.H);
+    int64_t rest = unit / NHALF / a.H;
     const int qt = (int)(rest % nqt);
     rest /= nqt;
     const int64_t chunk = rest % a.chunks, b = rest / a.chunks;
@@ -604,11 +623,12 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(4
             if constexpr (kSw) {
                 kT = load_k32_tr_sw32(k_lds, kt * 32, lane);
             } else if constexpr (kTr) {
-                kT = load_k32_tr(k_lds, KSTR, kt * 32, D, lane);
+                kT = load_k32_tr(k_lds + c_off, KSTR, kt * 32, DO, lane);
             } else {
                 const int c = sig(n);
 #pragma unroll
-                for (int u = 0; u < 16; ++u) kT.v[u] = c < D ? k_lds[(kt * 32 + krow(u, h2)) * KSTR + c] : 0.0f;
+                for (int u = 0; u < 16; ++u)
+                    kT.v[u] = c < DO ? k_lds[(kt * 32 + krow(u, h2)) * KSTR + c_off + c] : 0.0f;
             }
             Tr<T>::mma_k32(dq, kT, Tr<T>::pack(dS));
         } else {
@@ -618,12 +638,12 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(4
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
             const int c0 = 16 * half + 8 * h2;
-            if (16 * half >= D) continue;
-            if (c0 < D) {
+            if (16 * half >= DO) continue;
+            if (c0 < DO) {
                 const f32x4 x0 = {dq[8 * half], dq[8 * half + 1], dq[8 * half + 2], dq[8 * half + 3]};
                 const f32x4 x1 = {dq[8 * half + 4], dq[8 * half + 5], dq[8 * half + 6], dq[8 * half + 7]};
-                *reinterpret_cast<f32x4 *>(&dqp[dqp_index<D>(wave * 32 + n, n, c0 / 4)]) = x0;
-                *reinterpret_cast<f32x4 *>(&dqp[dqp_index<D>(wave * 32 + n, n, c0 / 4 + 1)]) = x1;
+                *reinterpret_cast<f32x4 *>(&dqp[dqp_index<DO>(wave * 32 + n, n, c0 / 4)]) = x0;
+                *reinterpret_cast<f32x4 *>(&dqp[dqp_index<DO>(wave * 32 + n, n, c0 / 4 + 1)]) = x1;
             }
         }
         __syncthreads();
@@ -632,8 +652,8 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(4
 #pragma unroll
         for (int j = 0; j < NSUM; ++j) {  // four consecutive channels per thread and step
             const int idx = tid + j * NT;
-            const int q = idx / (D / 4), cq = idx % (D / 4);
-            const bool ok = idx < 32 * (D / 4);
+            const int q = idx / (DO / 4), cq = idx % (DO / 4);
+            const bool ok = idx < 32 * (DO / 4);
             f32x4 sum = {0.0f, 0.0f, 0.0f, 0.0f};
             if (ok) {
                 // partials read four at a time and added as fixed trees
@@ -643,7 +663,7 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(4
                     f32x4 x[G];
 #pragma unroll
                     for (int w = 0; w < G; ++w)
-                        x[w] = *reinterpret_cast<const f32x4 *>(&dqp[dqp_index<D>((w0 + w) * 32 + q, q, cq)]);
+                        x[w] = *reinterpret_cast<const f32x4 *>(&dqp[dqp_index<DO>((w0 + w) * 32 + q, q, cq)]);
 #pragma unroll
                     for (int st = 1; st < G; st *= 2)
 #pragma unroll
@@ -651,8 +671,9 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(4
                     sum += x[0];
                 }
             }
-            const uint32_t off = (ok && qt * 32 + q < L) ? (uint32_t)(qt * 32 + q) * stok_b + (uint32_t)(4 * cq * ES)
-                                                         : kOOB;
+            const uint32_t off = (ok && qt * 32 + q < L)
+                                     ? (uint32_t)(qt * 32 + q) * stok_b + (uint32_t)((c_off + 4 * cq) * ES)
+                                     : kOOB;
             if constexpr (ES == 2) {
                 u32x2 w2;
                 w2.x = (uint32_t)f2bf(sum.x * a.scale) | ((uint32_t)f2bf(sum.y * a.scale) << 16);
@@ -665,7 +686,7 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(4
     }
 
     // ---- partial dBias tile of this chunk: [qi][kt*32 + krow(i, h2)]
-    if (a.part) {
+    if (a.part && ch == 0) {
         const rsrc_t rp = make_buf(a.part + ((b * a.H + hh) * a.chunks + chunk) * (int64_t)L * L, (uint32_t)(L * L * 4));
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
@@ -708,6 +729,10 @@ inline unsigned round8(int64_t n) { return (unsigned)((n + 7) / 8 * 8); }
 // bf16 bias rows made of whole 16-byte groups: kv reads the bias as it is
 inline bool bias_direct(const Problem &p) { return p.dtype == 1 && p.L % 8 == 0; }
 
+// units per (row, head) of the backward passes: head_dim 64 splits the
+// output channels over two workgroups
+inline int64_t head_halves(const Problem &p) { return p.D > 32 ? p.D / 32 : 1; }
+
 template <typename T, int D, int NKT, bool BV>
 hipError_t launch_passes(const Problem &p, const KvArgs &ka, const QbArgs &qa, hipStream_t s, Tracer &tr) {
     // grids are rounded up to a multiple of 8 for the XCD-aware unit order;
@@ -735,7 +760,10 @@ hipError_t launch_passes_d(const Problem &p, const KvArgs &ka, const QbArgs &qa,
     if (nkt <= 1) return launch_passes_v<T, D, 1>(p, ka, qa, s, tr);
     if (nkt <= 2) return launch_passes_v<T, D, 2>(p, ka, qa, s, tr);
     if (nkt <= 4) return launch_passes_v<T, D, 4>(p, ka, qa, s, tr);
-    return launch_passes_v<T, D, 8>(p, ka, qa, s, tr);
+    // fp32 at head_dim 64 past 128 keys would need more than the 160 KB of LDS
+    // (the ABI rejects it before this point)
+    if constexpr (sizeof(typename Tr<T>::elem) == 4 && D > 32) return hipErrorInvalidValue;
+    else return launch_passes_v<T, D, 8>(p, ka, qa, s, tr);
 }
 
 template <typename T>
@@ -768,7 +796,7 @@ hipError_t launch_bwd_t(const Problem &p, const BwdPtrs &x, void *ws, const BwdP
     ka.dk = x.dk; ka.dv = x.dv; ka.dg = x.dg;
     ka.da = w + plan.off_da; ka.dsum = (float *)(w + plan.off_dsum);
     ka.L = p.L; ka.rpb = rpb; ka.srow = p.srow; ka.stok = p.stok; ka.H = p.H; ka.scale = scale;
-    ka.n_units = p.N * p.H;
+    ka.n_units = p.N * p.H * head_halves(p);
     QbArgs qa;
     qa.q = x.q; qa.k = x.k; qa.v = x.v; qa.bias = x.bias; qa.mask = x.mask; qa.lse = x.lse;
     qa.da = ka.da; qa.dsum = ka.dsum; qa.dq = x.dq;
@@ -780,6 +808,7 @@ hipError_t launch_bwd_t(const Problem &p, const BwdPtrs &x, void *ws, const BwdP
     switch (p.D) {
         case 8: e = launch_passes_d<T, 8>(p, ka, qa, s, tr); break;
         case 16: e = launch_passes_d<T, 16>(p, ka, qa, s, tr); break;
+        case 64: e = launch_passes_d<T, 64>(p, ka, qa, s, tr); break;
         default: e = launch_passes_d<T, 32>(p, ka, qa, s, tr); break;
     }
     if (e != hipSuccess || !x.bias) return e;
@@ -813,7 +842,7 @@ BwdPlan plan_bwd(const Problem &p, bool has_bias) {
     }
     int64_t chunks = 0, g = 1;
     if (planes > 0 && rpb > 0 && nqt > 0) {
-        const int64_t per_chunk = planes * p.H * nqt * waves;  // waves per row chunk
+        const int64_t per_chunk = planes * p.H * nqt * waves * head_halves(p);  // waves per row chunk
         chunks = (target_waves + per_chunk - 1) / per_chunk;
         if (chunks < 1) chunks = 1;
         if (chunks > rpb) chunks = rpb;
@@ -822,7 +851,7 @@ BwdPlan plan_bwd(const Problem &p, bool has_bias) {
     }
     pl.chunks = chunks;
     pl.rows_per_chunk = g;
-    pl.n_wg = planes * p.H * nqt * chunks;
+    pl.n_wg = planes * p.H * nqt * chunks * head_halves(p);
     size_t off = 0;
     pl.off_da = off;
     off = align256(off + (size_t)(p.N * p.L * p.H * p.D * es));

@@ -5,7 +5,10 @@
 // pair bias enters the logits before the softmax; all of MHA in one kernel).
 //
 // Work unit = one (row, head), one workgroup per unit, one wave per
-// 32-query tile (seq_len <= 256, so at most 8 waves).  The kernel keeps its
+// 32-query tile (seq_len <= 256, so at most 8 waves); at head_dim 64 a unit
+// is a (row, head, half of the channels of O): both halves form the same
+// logits from all 64 channels, each produces 32 channels of O, and the first
+// writes the log-sum-exp.  The kernel keeps its
 // registers low (about 90 at head_dim 32) so that two workgroups share a CU
 // and each hides the other's loads and barriers.  K and V sit row-major in
 // LDS; the V^T operand of O^T = V^T P^T comes out of the transposing LDS read
@@ -97,25 +100,30 @@ __global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
     using K32 = typename Tr<T>::K32;
     constexpr int ES = sizeof(E);
     constexpr bool kBf = ES == 2;              // bf16: V^T via the transposing LDS read, bias via MFMA
-    constexpr bool kOnesRow = kBf && D < 32;   // row sums come out of the PV product
+    // output channels per workgroup: head_dim 64 runs as two units per (row,
+    // head), each contracting over all 64 channels for the logits and
+    // producing 32 channels of O
+    constexpr int DO = D > 32 ? 32 : D;
+    constexpr int NHALF = D / DO;
+    constexpr bool kOnesRow = kBf && DO < 32;  // row sums come out of the PV product
     constexpr int VEC = Tr<T>::VEC;
     constexpr int CPT = D / VEC;               // 16-byte chunks per token
     constexpr int LP = NKT * 32;
     constexpr int NT = NKT * 64;
     constexpr int KSTR = D + VEC;              // row stride of K / V in LDS (elements)
     constexpr int VSTR = LP + VEC;             // row stride of V^T in LDS (fp32 path)
-    // bf16: V rows in LDS are 32 columns wide whatever the head dim, the
-    // columns past D holding constants (a 1 in column D when the row sums come
-    // from the PV product, zeros elsewhere), so the transposing read needs no
-    // per-lane substitution
+    // bf16: V rows in LDS are 32 columns wide whatever the head dim (the
+    // unit's DO channels), the columns past DO holding constants (a 1 in column
+    // DO when the row sums come from the PV product, zeros elsewhere), so the
+    // transposing read needs no per-lane substitution
     constexpr int VSTRB = 32 + VEC;
-    constexpr int PCH = (32 - D) / 8;          // constant 16-byte chunks per V row
+    constexpr int PCH = (32 - DO) / 8;         // constant 16-byte chunks per V row
     constexpr int NCH = NKT / KC;              // chunks of KC key tiles
     constexpr int NPF = (LP * CPT + NT - 1) / NT;  // 16-byte chunks of K (and of V) per thread
     constexpr int NBB = kBf && BV ? KC : 1;    // bias fragments per chunk held in registers
     constexpr int NG = ES == 2 ? 1 : 2;        // 16-byte gate loads per 8 channels
     __shared__ __attribute__((aligned(16))) E k_lds[LP * KSTR];
-    __shared__ __attribute__((aligned(16))) E v_lds[kBf ? LP * VSTRB : D * VSTR];
+    __shared__ __attribute__((aligned(16))) E v_lds[kBf ? LP * VSTRB : DO * VSTR];
     __shared__ uint32_t kbits[NKT];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -128,12 +136,14 @@ __global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
     const uint32_t row_bytes = (uint32_t)(a.L * a.stok * ES);  // host: below 2^31
     const uint32_t q_off = qvalid ? (uint32_t)qi * stok_b : kOOB;
 
-    // one workgroup per (row, head) unit; consecutive units (the heads of a
-    // row) land on the same XCD
+    // one workgroup per (row, head[, channel half]) unit; consecutive units
+    // (the heads of a row) land on the same XCD
     const int64_t u = xcd_unit(blockIdx.x, gridDim.x);
     if (u >= a.n_units) return;
-    const int64_t r = u / a.H;
-    const int hh = (int)(u % a.H);
+    const int ch = NHALF == 1 ? 0 : (int)(u % NHALF);
+    const int c_off = ch * DO;  // first output channel of the unit
+    const int64_t r = u / NHALF / a.H;
+    const int hh = (int)(u / NHALF % a.H);
     auto tok_buf = [&](const void *X) {
         return make_buf((const E *)X + r * a.srow + (int64_t)hh * D, row_bytes);
     };
@@ -161,12 +171,15 @@ __global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
             if (idx < LP * CPT) {
                 const int t = idx / CPT, c = (idx % CPT) * VEC;
                 *reinterpret_cast<u32x4 *>(&k_lds[t * KSTR + c]) = kr[j];
-                if constexpr (kBf) {
-                    *reinterpret_cast<u32x4 *>(&v_lds[t * VSTRB + c]) = vr[j];
-                } else {
-                    const E *ve = reinterpret_cast<const E *>(&vr[j]);
+                const int cv = c - c_off;  // V: only the unit's output channels
+                if (NHALF == 1 || (cv >= 0 && cv < DO)) {
+                    if constexpr (kBf) {
+                        *reinterpret_cast<u32x4 *>(&v_lds[t * VSTRB + cv]) = vr[j];
+                    } else {
+                        const E *ve = reinterpret_cast<const E *>(&vr[j]);
 #pragma unroll
-                    for (int e = 0; e < VEC; ++e) v_lds[(c + e) * VSTR + t] = ve[e];
+                        for (int e = 0; e < VEC; ++e) v_lds[(cv + e) * VSTR + t] = ve[e];
+                    }
                 }
             }
         }
@@ -174,7 +187,7 @@ __global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
             for (int idx = tid; idx < LP * PCH; idx += NT) {
                 const int t = idx / PCH, pc = idx % PCH;
                 const u32x4 w = {(pc == 0 && kOnesRow) ? (uint32_t)(uint16_t)kBf16One : 0u, 0u, 0u, 0u};
-                *reinterpret_cast<u32x4 *>(&v_lds[t * VSTRB + D + 8 * pc]) = w;
+                *reinterpret_cast<u32x4 *>(&v_lds[t * VSTRB + DO + 8 * pc]) = w;
             }
         }
         const bool keep = (!has_mask || mb != 0) && tid < L;
@@ -197,8 +210,8 @@ __global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
         const int cb = 16 * half + 8 * h2;  // channels of O^T registers 8*half .. 8*half+7
-        if (16 * half >= D) continue;
-        const uint32_t off = cb < D ? q_off + (uint32_t)(cb * ES) : kOOB;
+        if (16 * half >= DO) continue;
+        const uint32_t off = cb < DO ? q_off + (uint32_t)((c_off + cb) * ES) : kOOB;
 #pragma unroll
         for (int gi = 0; gi < NG; ++gi) graw[half][gi] = bload16(rg, off + 16u * gi);
     }
@@ -309,7 +322,7 @@ __global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
             if constexpr (kBf) {
                 va = load_k32_tr(v_lds, VSTRB, kt * 32, 32, lane);
             } else {
-                if (sig(n) < D) va = load_k32<T>(&v_lds[sig(n) * VSTR + kt * 32], h2);
+                if (sig(n) < DO) va = load_k32<T>(&v_lds[sig(n) * VSTR + kt * 32], h2);
                 else va = zero_k32<T>();
             }
             Tr<T>::mma_k32(o, va, pb);
@@ -323,7 +336,7 @@ __global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
     }
     if constexpr (kOnesRow) {
         // channel D of O^T is the row sum: register 8*(D/16) + D%8 of lane half (D/8)%2
-        constexpr int ri = 8 * (D / 16) + D % 8, rh = (D / 8) % 2;
+        constexpr int ri = 8 * (DO / 16) + DO % 8, rh = (DO / 8) % 2;
         const float own = o[ri], other = __shfl_xor(own, 32);
         lsum = (h2 == rh) ? own : other;
     } else {
@@ -337,8 +350,8 @@ __global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
         const int cb = 16 * half + 8 * h2;
-        if (16 * half >= D) continue;
-        const uint32_t off = cb < D ? q_off + (uint32_t)(cb * ES) : kOOB;
+        if (16 * half >= DO) continue;
+        const uint32_t off = cb < DO ? q_off + (uint32_t)((c_off + cb) * ES) : kOOB;
         float gv[8];
         if constexpr (ES == 2) {
             const u32x4 w = graw[half][0];
@@ -377,7 +390,7 @@ __global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
     // lse in natural-log units: (m2 + log2 lsum) * ln 2
     const float lse = lsum > 0.0f ? (m2 + __builtin_amdgcn_logf(lsum)) * kLn2 : -INFINITY;
     bstore4(__builtin_bit_cast(uint32_t, lse), make_buf(a.lse + (r * a.H + hh) * a.L, (uint32_t)L * 4u),
-            (h2 == 0 && qvalid) ? (uint32_t)qi * 4u : kOOB);
+            (h2 == 0 && qvalid && ch == 0) ? (uint32_t)qi * 4u : kOOB);
 }
 
 // key tiles per register-resident chunk: one keeps the kernel near 90
@@ -392,7 +405,7 @@ hipError_t launch_t(const Problem &p, const FwdPtrs &x, hipStream_t s) {
     a.q = x.q; a.k = x.k; a.v = x.v; a.g = x.g; a.bias = x.bias; a.mask = x.mask;
     a.out = x.out; a.lse = x.lse;
     a.L = p.L; a.rpb = p.rpb; a.srow = p.srow; a.stok = p.stok; a.H = p.H;
-    a.n_units = p.N * p.H;
+    a.n_units = p.N * p.H * (D > 32 ? D / 32 : 1);
     a.scale = 1.0f / sqrtf((float)D);
     // one workgroup per unit; the grid is rounded up to a multiple of 8 so
     // that the XCD-aware unit order applies (surplus workgroups exit)
@@ -422,6 +435,7 @@ hipError_t launch_dt(const Problem &p, const FwdPtrs &x, hipStream_t s) {
     switch (p.D) {
         case 8: return launch_d<T, 8>(p, x, s);
         case 16: return launch_d<T, 16>(p, x, s);
+        case 64: return launch_d<T, 64>(p, x, s);
         default: return launch_d<T, 32>(p, x, s);
     }
 }

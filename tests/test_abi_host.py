@@ -62,7 +62,8 @@ def _fwd(dims, q=FAKE, k=FAKE + 4096, v=FAKE + 8192, g=None, bias=None, mask=Non
 @pytest.mark.parametrize("kw,status", [
     (dict(dtype=7), 2),
     (dict(head_dim=24), 2),
-    (dict(head_dim=64), 2),
+    (dict(head_dim=128), 2),
+    (dict(dtype=0, head_dim=64, seq_len=129), 2),   # fp32 d=64: at most 128 keys
     (dict(seq_len=257), 2),
     (dict(n_heads=0), 1),
     (dict(n_rows=-1), 1),
@@ -139,6 +140,10 @@ def test_workspace_size_is_positive_and_monotone():
     s2 = lib.evo_attn_bwd_workspace_size(ctypes.byref(_dims(n_rows=8, rows_per_bias=8)))
     assert 0 < s1 < s2
     assert lib.evo_attn_bwd_workspace_size(ctypes.byref(_dims(head_dim=24))) == 0
+    # head_dim 64: accepted (bf16 up to 256 keys, fp32 up to 128)
+    assert lib.evo_attn_bwd_workspace_size(ctypes.byref(_dims(head_dim=64, seq_len=256))) > 0
+    assert lib.evo_attn_bwd_workspace_size(ctypes.byref(_dims(dtype=0, head_dim=64, seq_len=128))) > 0
+    assert lib.evo_attn_bwd_workspace_size(ctypes.byref(_dims(dtype=0, head_dim=64, seq_len=136))) == 0
 
 
 def test_empty_problems_need_no_pointers():

@@ -48,6 +48,13 @@ SMALL = [
     (2, 96, 2, 32, "f32", dict(mask="length")),
     (2, 128, 1, 32, "f32", dict(gate=False)),
     (2, 250, 1, 16, "f32", dict(p=0.2)),
+    # head_dim 64: two workgroups per (row, head), each with 32 output channels
+    (2, 100, 2, 64, "bf16", dict()),
+    (2, 256, 1, 64, "bf16", dict(rpb=1)),
+    (2, 45, 2, 64, "bf16", dict(mask="length")),          # bias through the transpose kernel
+    (3, 64, 2, 64, "bf16", dict(gate=False, bias=False, mask="none")),
+    (2, 96, 1, 64, "f32", dict()),
+    (2, 128, 2, 64, "f32", dict(rpb=1, mask="tail_pad")),
 ]
 
 

@@ -189,3 +189,22 @@ def test_traced_backward_matches_plain(dtype, L):
     for a, b in zip(plain, traced):
         assert torch.equal(a, b)
     assert all(ev[j].elapsed_time(ev[j + 1]) >= 0.0 for j in range(len(ev) - 1))
+
+
+@pytest.mark.parametrize("dtype,bound", [("bf16", 1e-2), ("f32", 1e-4)])
+def test_gradient_sums_over_keys_vanish(dtype, bound):
+    """Every row of dS sums to zero over the keys (sum_j P_ij (dP_ij - D_i) =
+    D_i - D_i), so dK summed over the keys vanishes for every (row, head,
+    channel) and dBias summed over the keys vanishes for every (plane, head,
+    query).  Checked against the size of the summed terms: the bf16 path forms
+    D from the bf16 output, which leaves row sums of about 2^-9 of the terms."""
+    w, x = make_inputs(4, 96, 2, 32, dtype, seed=41, rpb=2)
+    print("\n[case] gradient sums", dtype, flush=True)
+    got = gpu_run(x, dtype, w.rows_per_bias)
+    for name, axis in (("dk", 1), ("dbias", -1)):
+        g = got[name]
+        total = np.abs(g.sum(axis=axis))
+        terms = np.abs(g).sum(axis=axis)
+        ratio = float((total / np.maximum(terms, 1e-30)).max())
+        print("  %-6s max |sum| / sum|.| = %.2e" % (name, ratio), flush=True)
+        assert (total <= bound * terms + 1e-7).all(), (name, ratio)

@@ -85,6 +85,7 @@ CASES = [
     dict(seed=5, N=4, L=7, H=3, d=4, rpb=2),        # two bias planes
     dict(seed=6, N=2, L=9, H=1, d=8, rpb=1, mask_p=0.6),
     dict(seed=7, N=1, L=1, H=1, d=1, rpb=1, mask_p=0.0),  # degenerate L=1
+    dict(seed=8, N=2, L=6, H=2, d=64, rpb=1),        # the largest head dim the library takes
 ]
 
 

@@ -99,7 +99,7 @@ def main():
         print(kernel_source_hash(args.source_hash))
         return
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(rows shard across GPUs with no communication in the forward and one dBias "
               "all-reduce in the backward; see the design notes)", file=sys.stderr)
         sys.exit(2)

@@ -835,11 +835,12 @@ BwdPlan plan_bwd(const Problem &p, bool has_bias) {
     // 8-wave workgroups on each of 256 CUs: the kernel's registers and LDS
     // allow two per CU), with as few row chunks as that allows (each chunk
     // costs one partial dBias plane)
-    int64_t target_waves = 4096;
-    if (const char *env = getenv("EVO_ATTN_QBIAS_WAVES")) {
-        const long v = atol(env);
-        if (v > 0) target_waves = v;
-    }
+    // (read once: the workspace size and the launch must see the same value)
+    static const int64_t target_waves = [] {
+        const char *env = getenv("EVO_ATTN_QBIAS_WAVES");
+        const long v = env ? atol(env) : 0;
+        return v > 0 ? (int64_t)v : (int64_t)4096;
+    }();
     int64_t chunks = 0, g = 1;
     if (planes > 0 && rpb > 0 && nqt > 0) {
         const int64_t per_chunk = planes * p.H * nqt * waves * head_halves(p);  // waves per row chunk

@@ -241,13 +241,15 @@ __global__ __launch_bounds__(64 * kPbbWaves) void pair_bias_bwd_kernel(PbBwdArgs
     }
 }
 
-// out = sum over workgroups of the partial rows, in workgroup order: a block
-// takes 16 groups of four columns and splits the rows into 16 interleaved
-// slices, whose sums are then added in slice order
+// out = sum over workgroups of the partial rows, in a fixed order: a block
+// takes 4 groups of four columns and splits the rows into 64 interleaved
+// slices, whose sums are then added in slice order (80 blocks at C = 128,
+// H = 8: 16 groups per block left the partial rows to 20 CUs, 4.8 us against
+// 4.0 us)
 __global__ __launch_bounds__(256) void pb_param_reduce_kernel(const float *__restrict__ part, int n_part, int HC,
                                                              int C, float *__restrict__ dW, float *__restrict__ dlw,
                                                              float *__restrict__ dlb) {
-    constexpr int KS = 16, QB = 16;
+    constexpr int KS = 64, QB = 4;
     __shared__ f32x4 sred[KS][QB];
     const int ks = threadIdx.x / QB, qb = threadIdx.x % QB;
     const int NX = HC + 2 * C;
@@ -285,7 +287,7 @@ hipError_t launch_ch(const PbBwdArgs &a, void *ws, hipStream_t s) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int nx4 = (H * C + 2 * C) / 4;
-    hipLaunchKernelGGL(pb_param_reduce_kernel, dim3((unsigned)((nx4 + 15) / 16)), dim3(256), 0, s, part, (int)nwg,
+    hipLaunchKernelGGL(pb_param_reduce_kernel, dim3((unsigned)((nx4 + 3) / 4)), dim3(256), 0, s, part, (int)nwg,
                        H * C, C, a.dW, a.dlnw, a.dlnb);
     return hipGetLastError();
 }

@@ -191,7 +191,7 @@ def test_traced_backward_matches_plain(dtype, L):
     assert all(ev[j].elapsed_time(ev[j + 1]) >= 0.0 for j in range(len(ev) - 1))
 
 
-@pytest.mark.parametrize("dtype,bound", [("bf16", 1e-2), ("f32", 1e-4)])
+@pytest.mark.parametrize("dtype,bound", [("bf16", 1e-2), ("f32", 1e-5)])
 def test_gradient_sums_over_keys_vanish(dtype, bound):
     """Every row of dS sums to zero over the keys (sum_j P_ij (dP_ij - D_i) =
     D_i - D_i), so dK summed over the keys vanishes for every (row, head,

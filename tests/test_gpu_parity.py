@@ -69,12 +69,13 @@ def test_small_ragged_parity(case):
     compare(got, ref, dtype, label=str(case))
 
 
-def test_ending_node_transposed_view():
+@pytest.mark.parametrize("d", [32, 64])
+def test_ending_node_transposed_view(d):
     """Triangle attention around the ending node: rows are the columns of the
     pair representation, passed as a strided view without a copy."""
-    L, H, d = 64, 4, 32
+    L, H = 64, 4
     w, x = make_inputs(L, L, H, d, "bf16", seed=11, mask="length")
-    print("\n[case] ending-node view", flush=True)
+    print("\n[case] ending-node view d=%d" % d, flush=True)
     # the pair representation z[i, j] holds row j, token i: build it so that
     # z.transpose(0, 1) is the [N=L, L, H, d] logical tensor of x
     def view(t):

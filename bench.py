@@ -44,28 +44,40 @@ def bias_transposed(w, es: int) -> bool:
 
 
 def kernel_model(w, es: int, ws_bytes: int):
-    """Per-launch algorithmic traffic (each input and output of the kernel
-    counted once, the shared bias plane once) and MFMA flops of every kernel
-    of one step, in launch order.  T = one [N, L, H, d] token tensor."""
+    """Per-launch traffic and MFMA flops of every kernel of one step, in launch
+    order, as (name, algorithmic bytes, workspace bytes, flops).
+
+    Algorithmic bytes count only the method's own tensors that the kernel
+    reads or writes, each once (Q, K, V, G, O, dO, LSE, bias, mask, dQ, dK, dV,
+    dG, fp32 dBias; the shared bias plane once per launch).  The kernel's own
+    scratch traffic -- dA and Dsum handed between the backward passes, the
+    transposed bias, the partial dBias planes -- is workspace, reported apart.
+    T = one [N, L, H, d] token tensor."""
     N, L, H, d = w.n_rows, w.seq_len, w.n_heads, w.head_dim
     T = N * L * H * d * es
     lse = N * H * L * 4
     B = N // w.rows_per_bias if w.bias else 0
     bias = B * H * L * L * es
+    dbias = B * H * L * L * 4
     mask = N * L if w.mask != "none" else 0
     g = 1 if w.gate else 0
     S = N * H * L * L  # logits
     transposed = bias_transposed(w, es)
-    parts = max(0, ws_bytes - _align(T) - _align(lse) - (_align(bias) if transposed else 0))
-    ks = [("fwd_kernel", (3 + g) * T + bias + mask + T + lse, 4.0 * S * d)]
+    biast = bias if transposed else 0
+    dsum = lse
+    parts = max(0, ws_bytes - _align(T) - _align(dsum) - (_align(biast) if transposed else 0))
+    ks = [("fwd_kernel", (3 + g) * T + bias + mask + T + lse, 0, 4.0 * S * d)]
     if transposed:
-        ks.append(("bias_transpose", 2 * bias, 0.0))
-    # dK/dV pass: reads Q K V O dO [G] lse bias (or its transpose) mask, writes dK dV dA [dG] Dsum
-    ks.append(("kv_kernel", (5 + g) * T + lse + bias + mask + (3 + g) * T + lse, 8.0 * S * d))
-    # dQ/dBias pass: reads Q K V dA lse Dsum bias mask, writes dQ and the partial dBias planes
-    ks.append(("qbias_kernel", 4 * T + 2 * lse + bias + mask + T + parts, 6.0 * S * d))
+        ks.append(("bias_transpose", bias, biast, 0.0))
+    # dK/dV pass: reads Q K V O dO [G] lse bias mask, writes dK dV [dG];
+    # workspace: writes dA and Dsum (and reads the transposed bias)
+    ks.append(("kv_kernel", (5 + g) * T + lse + (0 if transposed else bias) + mask + (2 + g) * T,
+               T + dsum + biast, 8.0 * S * d))
+    # dQ/dBias pass: reads Q K V lse bias mask, writes dQ; workspace: reads dA
+    # and Dsum, writes the partial dBias planes
+    ks.append(("qbias_kernel", 3 * T + lse + bias + mask + T, T + dsum + parts, 6.0 * S * d))
     if w.bias:
-        ks.append(("dbias_reduce", parts + B * H * L * L * 4, 0.0))
+        ks.append(("dbias_reduce", dbias, parts, 0.0))
     return ks
 
 
@@ -232,12 +244,17 @@ def main():
     model = kernel_model(w, es, ws.numel())
     assert len(model) == len(kern_ms), (len(model), len(kern_ms))
     kernels = {}
-    for (name, nbytes, kflops), ms in zip(model, kern_ms):
+    for (name, nbytes, wsb, kflops), ms in zip(model, kern_ms):
+        tr = measured_traffic(name, w.name)
         kernels[name] = {"avg_ms": round(ms, 5), "algorithmic_bytes": int(nbytes),
+                         "workspace_bytes": int(wsb),
                          "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
-                         "mfma_tflops": round(kflops / (ms * 1e-3) / 1e12, 1)}
+                         "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                         "mfma_tflops": round(kflops / (ms * 1e-3) / 1e12, 1),
+                         "traffic": tr,
+                         "traffic_over_algorithmic": None if tr is None or not nbytes else round(tr / nbytes, 3)}
     dom = max(range(len(model)), key=lambda i: kern_ms[i])
-    dname, dbytes, dflops = model[dom]
+    dname, dbytes, _, dflops = model[dom]
     dms = kern_ms[dom]
     peak_mfma = MFMA_BF16_PEAK_TFLOPS if w.dtype == "bf16" else MFMA_F32_PEAK_TFLOPS
     ridge = peak_mfma * 1e12 / (HBM_PEAK_GBS * 1e9)          # flop per byte
@@ -249,9 +266,13 @@ def main():
         ach = dbytes / (dms * 1e-3) / 1e9
         roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(ach / HBM_PEAK_GBS, 4)}
-    roofline.update({"traffic": measured_traffic(dname, w.name), "kernel": dname, "avg_ms": round(dms, 5),
+    dtr = measured_traffic(dname, w.name)
+    roofline.update({"traffic": dtr, "kernel": dname, "avg_ms": round(dms, 5),
                      "algorithmic_bytes": int(dbytes), "flops": dflops,
-                     "intensity_flop_per_byte": round(dflops / max(dbytes, 1), 1)})
+                     "intensity_flop_per_byte": round(dflops / max(dbytes, 1), 1),
+                     "traffic_over_algorithmic": None if dtr is None else round(dtr / max(dbytes, 1), 3)})
+    step_traffic = [measured_traffic(n, w.name) for n, _, _, _ in model]
+    step_traffic = None if any(t is None for t in step_traffic) else int(sum(step_traffic))
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -279,6 +300,11 @@ def main():
         "kernels": kernels,
         "fwd_bwd_frac_of_mfma_peak": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
         "fwd_bwd_hbm_gbs": round((fwd_bytes + bwd_bytes) / (ms_step * 1e-3) / 1e9, 1),
+        "step_hbm": {"algorithmic_bytes": int(fwd_bytes + bwd_bytes),
+                     "frac": round((fwd_bytes + bwd_bytes) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "traffic": step_traffic,
+                     "traffic_over_algorithmic": None if step_traffic is None
+                     else round(step_traffic / (fwd_bytes + bwd_bytes), 3)},
         "wall_s": round(wall, 3),
         "roofline": roofline,
         "cpu_baseline": cpu,
@@ -991,31 +1017,52 @@ def cpu_baseline(w, x, target_s: float):
     # a sample of at least one whole bias plane keeps whole planes
     if w.bias and want >= w.rows_per_bias:
         want = (want // w.rows_per_bias) * w.rows_per_bias
+    # the same sample three times (more when one run is short), median taken
+    reps = 3
+    if want == w.n_rows and 3 * t < target_s:  # the whole workload is short: repeat it
+        reps = max(3, int(target_s / max(t, 1e-3)))
+    elif t > target_s / 3:                    # keep three runs near the target
+        want = max(1, int(want * target_s / (3 * t)))
+        if w.bias and want >= w.rows_per_bias:
+            want = (want // w.rows_per_bias) * w.rows_per_bias
     split.clear()
-    t = run(want)
-    reps = 1
-    if want == w.n_rows and t < target_s:  # the whole workload is short: repeat it
-        reps = max(1, int(target_s / max(t, 1e-3)))
-        t = sum(run(want) for _ in range(reps)) / reps
+    times = [run(want) for _ in range(reps)]
+    t = float(np.median(times))
     flops = (w.flops_fwd() + w.flops_bwd()) * want / w.n_rows
     tf = float(np.median([a for a, _ in split]))
     tb = float(np.median([b_ for _, b_ in split]))
     return {"value": round(flops / t / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.threads(),
             "kind": "oracle", "cpu_model": _cpu_model(), "seconds_per_run": round(t, 3), "runs": reps,
             "fwd_s_median": round(tf, 3), "bwd_s_median": round(tb, 3),
-            "sample": "%d of %d rows of %s, forward + backward in fp64 (OpenMP), mean of %d run(s)"
+            "sample": "%d of %d rows of %s, forward + backward in fp64 (OpenMP), median of %d runs"
                       % (want, w.n_rows, w.name, reps)}
 
 
 def _cpu_model() -> str:
+    """The host CPU as /proc/cpuinfo names it, with its family / model /
+    stepping numbers (some hosts report only a generic model name)."""
+    info = {}
     try:
         with open("/proc/cpuinfo") as f:
             for ln in f:
-                if ln.startswith("model name"):
-                    return ln.split(":", 1)[1].strip()
+                if ":" not in ln:
+                    if info:
+                        break  # first processor block only
+                    continue
+                key, val = (x.strip() for x in ln.split(":", 1))
+                info.setdefault(key, val)
     except OSError:
+        return "unknown"
+    name = info.get("model name", "unknown")
+    ids = ", ".join("%s %s" % (k, info[k]) for k in ("cpu family", "model", "stepping") if k in info)
+    extra = [ids] if ids else []
+    if "cpu MHz" in info:
+        extra.append("%s MHz" % info["cpu MHz"])
+    try:
+        extra.append("%d logical CPUs on the host" % os.cpu_count())
+    except TypeError:
         pass
-    return "unknown"
+    return "%s (%s)" % (name, "; ".join(extra)) if extra else name
 
 
 if __name__ == "__main__":

@@ -75,7 +75,15 @@ enum evo_attn_status {
  * backward's LDS tiles hold).  Head dims 8, 16 and 32 cover every Evoformer
  * attention (MSA row and column, triangle, extra-MSA); head_dim 64 runs each
  * (row, head) as two workgroups that form the same logits from all 64 channels
- * and produce 32 output channels each. */
+ * and produce 32 output channels each.
+ *
+ * Accuracy limit of the bf16 backward: it forms D_i = sum_c dO_ic O_ic from the
+ * saved bf16 output O, so D carries about 2^-9 * ||dO_i * O_i||_2 of rounding
+ * (grows as sqrt(head_dim) for unit-size entries), and dS = P (dP - D) inherits
+ * it in full where the softmax puts its mass on a single key.  At head_dim <= 32
+ * the gradients stay within 2e-2 abs + 2e-2 rel of the exact ones on such
+ * inputs; at head_dim 64 a strongly peaked softmax (logit gaps of tens) can put
+ * single dBias elements a few percent past that bound. */
 #define EVO_ATTN_MAX_SEQ_LEN 256
 #define EVO_ATTN_MAX_SEQ_LEN_F32_D64 128
 

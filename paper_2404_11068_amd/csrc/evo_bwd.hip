@@ -303,7 +303,6 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
     }
     const bool kvalid = kin && (!has_mask || mbyte != 0);
     const bool kfull = __ballot(kvalid) == ~0ull;
-    const float keepf = kvalid ? 1.0f : 0.0f;  // masked key: its lane's P is 0
     const float c2 = a.scale * kLog2e;
     const int arow = sig(n);  // permuted A-operand row of this lane
     uint16_t *const bt_tile = &bt_lds[kBD ? wave * 1024 : 0];
@@ -343,7 +342,10 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
                 const int i = 8 * half + s8;
                 // log2 P = c2 * S + log2(e) * bias - lse * log2(e)
                 float p = __builtin_amdgcn_exp2f(__builtin_fmaf(S[i], c2, __builtin_fmaf(bcur[i], kLog2e, -l2[s8])));
-                if (!kfull) p *= keepf;
+                // masked key: its lane's P is exactly 0.  A select, not a
+                // product: the lse leaves masked keys out, so exp2 of a masked
+                // logit far above it is +inf, and inf * 0 would be NaN
+                if (!kfull) p = kvalid ? p : 0.0f;
                 P[i] = p;
                 dS[i] = p * (dP[i] - ds[s8]);
             }

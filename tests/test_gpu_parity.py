@@ -88,7 +88,19 @@ def test_ending_node_transposed_view(d):
     compare(got, ref, "bf16", label="ending-node")
 
 
-@pytest.mark.parametrize("dtype,d", [("bf16", 32), ("bf16", 8), ("f32", 16)])
+# head_dim 64, bf16: the backward forms D_i = sum_c dO_ic o_ic from the
+# bf16-rounded output, so D carries about 2^-9 * ||dO_i o_i|| (sqrt(d) * 2^-9
+# for unit entries) of rounding, and dS = P (dP - D) inherits all of it where
+# P puts its mass on one key -- which is what this ramp does.  At d = 64 one
+# dBias element misses the element bound by about 5%; the limit is stated in
+# include/evo_attn.h.
+_D64_RAMP = pytest.mark.xfail(reason="bf16 head_dim 64: D is formed from the bf16 output; a peaked softmax "
+                                     "leaves dBias ~5% past the element bound (stated in evo_attn.h)",
+                              strict=False)
+
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 32), ("bf16", 8), ("f32", 16),
+                                     pytest.param("bf16", 64, marks=_D64_RAMP)])
 @pytest.mark.parametrize("sign", [1, -1])
 def test_running_max_moves(dtype, d, sign):
     """A bias ramp of 40 along the keys makes the logits of every query grow
@@ -127,6 +139,31 @@ def test_masked_keys_get_exact_zero_gradients():
     masked = x["mask"] == 0
     assert masked.any()
     assert (got["dk"][masked] == 0).all() and (got["dv"][masked] == 0).all()
+
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 8), ("bf16", 32), ("f32", 16)])
+def test_masked_keys_with_huge_logits(dtype, d):
+    """Masked keys whose logits sit more than 100 above every kept key's are
+    still excluded: exp of such a logit against the saved lse (which leaves
+    masked keys out) overflows to +inf, so any multiply-by-zero masking would
+    turn it into NaN.  One bias plane per row carries +120 at that row's
+    masked keys; dK, dV and dBias must be exactly 0 there, and every output
+    must match the oracle."""
+    N, L, H = 3, 90, 2
+    w, x = make_inputs(N, L, H, d, dtype, seed=55 + d, rpb=1, p=0.3)
+    masked = x["mask"] == 0
+    assert masked.any()
+    b = W.as_float64(x["bias"], dtype) + 120.0 * masked[:, None, None, :]
+    x = dict(x)
+    x["bias"] = W.f32_to_bf16_bits(b.astype(np.float32)) if dtype == "bf16" else b.astype(np.float32)
+    print("\n[case] masked keys, huge logits", dtype, d, flush=True)
+    got = gpu_run(x, dtype, w.rows_per_bias)
+    for n in ("dk", "dv"):
+        assert (got[n][masked] == 0).all(), n
+    db = got["dbias"]  # [N, H, L, L]: plane r belongs to row r, its last axis is the key
+    assert (db[np.broadcast_to(masked[:, None, None, :], db.shape)] == 0).all()
+    ref = oracle_run(x, dtype, w.rows_per_bias)
+    compare(got, ref, dtype, label="huge masked logits %s d%d" % (dtype, d))
 
 
 def test_empty_problems_are_noops():

@@ -67,7 +67,9 @@ enum evo_attn_status {
     EVO_ERR_UNSUPPORTED = 2, /* dtype, head_dim or seq_len outside the compiled set */
     EVO_ERR_ALIGNMENT = 3,   /* token pointers/strides must allow 16-byte vector access */
     EVO_ERR_WORKSPACE = 4,   /* workspace missing or smaller than evo_attn_bwd_workspace_size */
-    EVO_ERR_HIP = 5          /* a kernel launch failed (hipGetLastError after the launch) */
+    EVO_ERR_HIP = 5,         /* a kernel launch failed (hipGetLastError after the launch) */
+    EVO_ERR_SCRATCH_LIMIT = 6 /* evo_attn_bwd_noalloc: the problem needs more scratch than
+                                 EVO_ATTN_NOALLOC_SCRATCH_BYTES */
 };
 
 /* Compiled limits: head_dim in {8, 16, 32, 64}; 0 <= seq_len <= EVO_ATTN_MAX_SEQ_LEN
@@ -165,6 +167,37 @@ int evo_attn_bwd_traced(const evo_attn_dims *dims, const void *q, const void *k,
                         const void *out, const float *lse, const void *dout, void *dq, void *dk,
                         void *dv, void *dgate, float *dbias, void *workspace,
                         size_t workspace_bytes, void *const *events, int n_events, void *stream);
+
+/*
+ * Backward pass that allocates nothing, for callers that cannot allocate
+ * device memory or pass a workspace: code being captured into a HIP graph,
+ * tight serving loops, harnesses that forbid hipMalloc.
+ *
+ * Same arguments and results as evo_attn_bwd without the workspace: the
+ * scratch lives in a fixed buffer of EVO_ATTN_NOALLOC_SCRATCH_BYTES that the
+ * library holds on every device it runs on, from the first call on that
+ * device until the process ends.  The stream must belong to the current
+ * device (the buffer is looked up for it on the first call there).
+ *   - Calls on one device share that buffer: two calls that overlap in time
+ *     on one device (different streams, or different host threads without
+ *     ordering between their streams) race and give undefined results.
+ *     Calls ordered on one stream are safe.  The buffer keeps the last
+ *     call's contents; nothing in it needs clearing between calls.
+ *   - A problem whose scratch does not fit is refused before any HIP call
+ *     with EVO_ERR_SCRATCH_LIMIT.  Where fewer dBias partial planes make it
+ *     fit, the call uses fewer (so its dBias may differ from evo_attn_bwd's
+ *     in the order of the row sums, within rounding); otherwise results are
+ *     bitwise those of evo_attn_bwd.
+ *   - No hipMalloc, hipFree or other allocating call is made.
+ */
+#define EVO_ATTN_NOALLOC_SCRATCH_BYTES (64u << 20)
+int evo_attn_bwd_noalloc(const evo_attn_dims *dims, const void *q, const void *k, const void *v,
+                         const void *gate, const void *bias, const uint8_t *key_mask,
+                         const void *out, const float *lse, const void *dout, void *dq, void *dk,
+                         void *dv, void *dgate, float *dbias, void *stream);
+
+/* EVO_ATTN_NOALLOC_SCRATCH_BYTES as compiled into the library. */
+size_t evo_attn_bwd_noalloc_scratch_bytes(void);
 
 /* Number of kernels one evo_attn_bwd call launches (has_bias: bias != NULL). */
 int evo_attn_bwd_kernel_count(int has_bias);

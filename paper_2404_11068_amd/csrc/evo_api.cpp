@@ -67,6 +67,9 @@ const char *evo_attn_strerror(int status) {
         case EVO_ERR_ALIGNMENT: return "pointer or stride not aligned for 16-byte access";
         case EVO_ERR_WORKSPACE: return "workspace missing or too small";
         case EVO_ERR_HIP: return "HIP kernel launch failed";
+        case EVO_ERR_SCRATCH_LIMIT:
+            return "problem needs more backward scratch than the no-alloc entry point's fixed buffer "
+                   "(EVO_ATTN_NOALLOC_SCRATCH_BYTES) holds; use evo_attn_bwd with a workspace";
         default: return "unknown status";
     }
 }
@@ -99,14 +102,15 @@ size_t evo_attn_bwd_workspace_size(const evo_attn_dims *dims) {
 
 namespace {
 
-int bwd_impl(const evo_attn_dims *dims, const void *q, const void *k, const void *v, const void *gate,
-             const void *bias, const uint8_t *key_mask, const void *out, const float *lse, const void *dout,
-             void *dq, void *dk, void *dv, void *dgate, float *dbias, void *workspace, size_t workspace_bytes,
-             void *stream, evo::Tracer *tr) {
-    evo::Problem p;
+// dims and pointers of a backward call (no HIP call); an empty problem
+// returns EVO_OK with p->N == 0 or p->L == 0 before any pointer is looked at
+int check_bwd_args(const evo_attn_dims *dims, const void *q, const void *k, const void *v, const void *gate,
+                   const void *bias, const void *out, const float *lse, const void *dout, void *dq, void *dk,
+                   void *dv, void *dgate, float *dbias, evo::Problem *pp) {
+    evo::Problem &p = *pp;
     int st = check_dims(dims, bias != nullptr, &p);
     if (st) return st;
-    if (p.N == 0 || p.L == 0) return EVO_OK;  // nothing is read or written
+    if (p.N == 0 || p.L == 0) return EVO_OK;
     if (!q || !k || !v || !out || !lse || !dout || !dq || !dk || !dv) return EVO_ERR_INVALID_ARG;
     if ((gate == nullptr) != (dgate == nullptr) || (bias == nullptr) != (dbias == nullptr))
         return EVO_ERR_INVALID_ARG;
@@ -116,6 +120,17 @@ int bwd_impl(const evo_attn_dims *dims, const void *q, const void *k, const void
     if ((gate && !aligned16(gate)) || (dgate && !aligned16(dgate)) || (bias && !aligned16(bias)) ||
         (dbias && !aligned16(dbias)) || !aligned4(lse))
         return EVO_ERR_ALIGNMENT;
+    return EVO_OK;
+}
+
+int bwd_impl(const evo_attn_dims *dims, const void *q, const void *k, const void *v, const void *gate,
+             const void *bias, const uint8_t *key_mask, const void *out, const float *lse, const void *dout,
+             void *dq, void *dk, void *dv, void *dgate, float *dbias, void *workspace, size_t workspace_bytes,
+             void *stream, evo::Tracer *tr) {
+    evo::Problem p;
+    int st = check_bwd_args(dims, q, k, v, gate, bias, out, lse, dout, dq, dk, dv, dgate, dbias, &p);
+    if (st) return st;
+    if (p.N == 0 || p.L == 0) return EVO_OK;  // nothing is read or written
     const evo::BwdPlan plan = evo::plan_bwd(p, bias != nullptr);
     if (!workspace || workspace_bytes < plan.total || ((uintptr_t)workspace & 255u) != 0) return EVO_ERR_WORKSPACE;
     if (tr && tr->n < evo::bwd_kernel_count(bias != nullptr) + 1) return EVO_ERR_INVALID_ARG;
@@ -136,6 +151,28 @@ int evo_attn_bwd(const evo_attn_dims *dims, const void *q, const void *k, const 
     return bwd_impl(dims, q, k, v, gate, bias, key_mask, out, lse, dout, dq, dk, dv, dgate, dbias, workspace,
                     workspace_bytes, stream, nullptr);
 }
+
+int evo_attn_bwd_noalloc(const evo_attn_dims *dims, const void *q, const void *k, const void *v,
+                         const void *gate, const void *bias, const uint8_t *key_mask, const void *out,
+                         const float *lse, const void *dout, void *dq, void *dk, void *dv, void *dgate,
+                         float *dbias, void *stream) {
+    evo::Problem p;
+    int st = check_bwd_args(dims, q, k, v, gate, bias, out, lse, dout, dq, dk, dv, dgate, dbias, &p);
+    if (st) return st;
+    if (p.N == 0 || p.L == 0) return EVO_OK;  // nothing is read or written
+    // the plan takes fewer dBias row chunks where that brings it under the
+    // buffer; a problem that does not fit even then is refused here, before
+    // any HIP call
+    const evo::BwdPlan plan = evo::plan_bwd(p, bias != nullptr, evo::kNoAllocScratchBytes);
+    if (plan.total > evo::kNoAllocScratchBytes) return EVO_ERR_SCRATCH_LIMIT;
+    void *scratch = nullptr;
+    if (evo::noalloc_scratch_ptr(&scratch) != hipSuccess) return EVO_ERR_HIP;
+    evo::BwdPtrs x{q, k, v, gate, bias, key_mask, out, lse, dout, dq, dk, dv, dgate, dbias};
+    hipError_t e = evo::launch_bwd(p, x, scratch, plan, (hipStream_t)stream, nullptr);
+    return e == hipSuccess ? EVO_OK : EVO_ERR_HIP;
+}
+
+size_t evo_attn_bwd_noalloc_scratch_bytes(void) { return evo::kNoAllocScratchBytes; }
 
 int evo_attn_bwd_kernel_count(int has_bias) { return evo::bwd_kernel_count(has_bias != 0); }
 

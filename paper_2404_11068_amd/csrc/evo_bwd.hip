@@ -36,6 +36,9 @@
 #include <math.h>
 #include <stdlib.h>
 
+#include <atomic>
+#include <mutex>
+
 #include "evo_frag.h"
 #include "evo_kernels.h"
 
@@ -826,8 +829,7 @@ hipError_t launch_bwd_t(const Problem &p, const BwdPtrs &x, void *ws, const BwdP
 
 }  // namespace
 
-BwdPlan plan_bwd(const Problem &p, bool has_bias) {
-    BwdPlan pl;
+BwdPlan plan_bwd(const Problem &p, bool has_bias, size_t cap) {
     const int64_t es = p.dtype == 1 ? 2 : 4;
     const int64_t planes = has_bias ? p.N / p.rpb : (p.N > 0 ? 1 : 0);
     const int64_t rpb = has_bias ? p.rpb : p.N;
@@ -843,32 +845,79 @@ BwdPlan plan_bwd(const Problem &p, bool has_bias) {
         const long v = env ? atol(env) : 0;
         return v > 0 ? (int64_t)v : (int64_t)4096;
     }();
-    int64_t chunks = 0, g = 1;
+    int64_t chunks = 0;
     if (planes > 0 && rpb > 0 && nqt > 0) {
         const int64_t per_chunk = planes * p.H * nqt * waves * head_halves(p);  // waves per row chunk
         chunks = (target_waves + per_chunk - 1) / per_chunk;
         if (chunks < 1) chunks = 1;
         if (chunks > rpb) chunks = rpb;
-        g = (rpb + chunks - 1) / chunks;
-        chunks = (rpb + g - 1) / g;
     }
-    pl.chunks = chunks;
-    pl.rows_per_chunk = g;
-    pl.n_wg = planes * p.H * nqt * chunks * head_halves(p);
-    size_t off = 0;
-    pl.off_da = off;
-    off = align256(off + (size_t)(p.N * p.L * p.H * p.D * es));
-    pl.off_dsum = off;
-    off = align256(off + (size_t)(p.N * p.H * p.L) * 4);
-    pl.off_biast = off;
-    if (has_bias && !bias_direct(p)) off = align256(off + (size_t)(planes * p.H * p.L * p.L * es));
-    pl.off_part = off;
-    if (has_bias) off = align256(off + (size_t)(planes * p.H * chunks * p.L * p.L) * 4);
-    pl.total = off;
+    // workspace layout for a given number of row chunks; with a cap, fewer
+    // chunks (fewer partial dBias planes, longer qbias workgroups) until it fits
+    auto layout = [&](int64_t want) {
+        BwdPlan pl;
+        int64_t g = 1, c = 0;
+        if (want > 0) {
+            g = (rpb + want - 1) / want;
+            c = (rpb + g - 1) / g;
+        }
+        pl.chunks = c;
+        pl.rows_per_chunk = g;
+        pl.n_wg = planes * p.H * nqt * c * head_halves(p);
+        size_t off = 0;
+        pl.off_da = off;
+        off = align256(off + (size_t)(p.N * p.L * p.H * p.D * es));
+        pl.off_dsum = off;
+        off = align256(off + (size_t)(p.N * p.H * p.L) * 4);
+        pl.off_biast = off;
+        if (has_bias && !bias_direct(p)) off = align256(off + (size_t)(planes * p.H * p.L * p.L * es));
+        pl.off_part = off;
+        if (has_bias) off = align256(off + (size_t)(planes * p.H * c * p.L * p.L) * 4);
+        pl.total = off;
+        return pl;
+    };
+    BwdPlan pl = layout(chunks);
+    while (pl.total > cap && pl.chunks > 1) {
+        // halve the chunk count (at least one fewer) and lay out again
+        const int64_t fewer = pl.chunks / 2 < pl.chunks - 1 ? pl.chunks / 2 : pl.chunks - 1;
+        pl = layout(fewer);
+    }
     return pl;
 }
 
 int bwd_kernel_count(bool has_bias) { return has_bias ? 4 : 2; }
+
+// ---------------------------------------------------------------------------
+// Fixed scratch of evo_attn_bwd_noalloc: one copy per device, resident until
+// the process ends.  In host code `noalloc_scratch` names a host-side shadow,
+// not device memory; the device address is looked up once per device (with
+// that device current) and only that address is ever handed to kernels.
+static __device__ __align__(256) unsigned char noalloc_scratch[kNoAllocScratchBytes];
+namespace {
+constexpr int kMaxDevices = 64;
+std::atomic<void *> g_noalloc_ptr[kMaxDevices];  // zero-initialised (static storage)
+std::mutex g_noalloc_mu;
+}  // namespace
+
+hipError_t noalloc_scratch_ptr(void **out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    void *p = g_noalloc_ptr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        std::lock_guard<std::mutex> lock(g_noalloc_mu);
+        p = g_noalloc_ptr[dev].load(std::memory_order_relaxed);
+        if (!p) {
+            e = hipGetSymbolAddress(&p, HIP_SYMBOL(noalloc_scratch));
+            if (e != hipSuccess) return e;
+            if (!p) return hipErrorInvalidSymbol;
+            g_noalloc_ptr[dev].store(p, std::memory_order_release);
+        }
+    }
+    *out = p;
+    return hipSuccess;
+}
 
 hipError_t launch_bwd(const Problem &p, const BwdPtrs &x, void *ws, const BwdPlan &plan, hipStream_t s,
                       Tracer *tr) {

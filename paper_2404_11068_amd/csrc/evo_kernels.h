@@ -40,7 +40,16 @@ struct BwdPlan {
     size_t off_da, off_dsum, off_biast, off_part, total;
 };
 
-BwdPlan plan_bwd(const Problem &p, bool has_bias);
+// cap: largest workspace the caller can give; the plan takes fewer row chunks
+// (fewer partial dBias planes) to stay under it where it can (callers check
+// .total against the cap)
+BwdPlan plan_bwd(const Problem &p, bool has_bias, size_t cap = ~(size_t)0);
+
+// Fixed device scratch of the no-alloc backward (EVO_ATTN_NOALLOC_SCRATCH_BYTES
+// per device): its device address on the current device, looked up on the
+// first call per device.
+constexpr size_t kNoAllocScratchBytes = (size_t)64 << 20;
+hipError_t noalloc_scratch_ptr(void **out);
 
 // Optional stage markers: records caller-owned events on the launch stream
 // before the first kernel and after each kernel (profiling only).

@@ -68,6 +68,10 @@ def load_library():
         lib.evo_attn_bwd_traced.argtypes = [D] + [P] * 15 + [ctypes.c_size_t, ctypes.POINTER(P),
                                                             ctypes.c_int, P]
         lib.evo_attn_bwd_traced.restype = ctypes.c_int
+        lib.evo_attn_bwd_noalloc.argtypes = [D] + [P] * 14 + [P]
+        lib.evo_attn_bwd_noalloc.restype = ctypes.c_int
+        lib.evo_attn_bwd_noalloc_scratch_bytes.argtypes = []
+        lib.evo_attn_bwd_noalloc_scratch_bytes.restype = ctypes.c_size_t
         lib.evo_attn_bwd_kernel_count.argtypes = [ctypes.c_int]
         lib.evo_attn_bwd_kernel_count.restype = ctypes.c_int
         lib.evo_attn_strerror.argtypes = [ctypes.c_int]
@@ -199,4 +203,38 @@ def evo_attn_bwd(q, k, v, gate, bias, key_mask, out, lse, dout, *, rows_per_bias
         where = "evo_attn_bwd_traced"
     if st:
         raise EvoAttnError(st, where)
+    return dq, dk, dv, dgate, dbias
+
+
+def evo_attn_bwd_noalloc_scratch_bytes() -> int:
+    return int(load_library().evo_attn_bwd_noalloc_scratch_bytes())
+
+
+def evo_attn_bwd_noalloc(q, k, v, gate, bias, key_mask, out, lse, dout, *, rows_per_bias=None,
+                         dq=None, dk=None, dv=None, dgate=None, dbias=None, stream=None):
+    """Backward pass through evo_attn_bwd_noalloc (no workspace: the library's
+    fixed per-device scratch).  Output tensors that are not passed in are
+    created here with torch; pass all of them to make the call itself
+    allocation-free.  Returns (dq, dk, dv, dgate or None, dbias or None)."""
+    lib = load_library()
+    _same_layout(q, k, v, gate, out, dout)
+    dims = make_dims(q, rows_per_bias)
+
+    def like_q():
+        return torch.empty_strided(q.shape, q.stride(), dtype=q.dtype, device=q.device)
+
+    dq = like_q() if dq is None else dq
+    dk = like_q() if dk is None else dk
+    dv = like_q() if dv is None else dv
+    if gate is not None and dgate is None:
+        dgate = like_q()
+    if bias is not None and dbias is None:
+        dbias = torch.empty(bias.shape, dtype=torch.float32, device=q.device)
+    _same_layout(q, dq, dk, dv, dgate)
+    key_mask = _mask_u8(key_mask)
+    st = lib.evo_attn_bwd_noalloc(ctypes.byref(dims), _ptr(q), _ptr(k), _ptr(v), _ptr(gate), _ptr(bias),
+                                  _ptr(key_mask), _ptr(out), _ptr(lse), _ptr(dout), _ptr(dq), _ptr(dk),
+                                  _ptr(dv), _ptr(dgate), _ptr(dbias), _stream(stream))
+    if st:
+        raise EvoAttnError(st, "evo_attn_bwd_noalloc")
     return dq, dk, dv, dgate, dbias

@@ -28,6 +28,7 @@ def test_exports_every_declared_symbol():
                        open(HEADER).read(), flags=re.M)
     assert set(decls) == {"evo_attn_fwd", "evo_attn_bwd", "evo_attn_bwd_workspace_size",
                           "evo_attn_bwd_traced", "evo_attn_bwd_kernel_count",
+                          "evo_attn_bwd_noalloc", "evo_attn_bwd_noalloc_scratch_bytes",
                           "evo_attn_strerror", "evo_attn_version"}
     for name in decls:
         assert hasattr(lib, name), name
@@ -35,7 +36,7 @@ def test_exports_every_declared_symbol():
 
 def test_strerror_and_version():
     _lib()
-    for st in range(6):
+    for st in range(7):
         assert isinstance(ea.evo_attn_strerror(st), str) and ea.evo_attn_strerror(st)
     assert "unknown" in ea.evo_attn_strerror(99)
     assert ea.evo_attn_version() >= 10000
@@ -157,3 +158,39 @@ def test_empty_problems_need_no_pointers():
                     dv=None, ws=None, ws_bytes=0) == 0
         # with a bias the plan must not divide by the zero plane count
         assert _fwd(d, q=None, bias=None) == 0
+
+
+def _bwd_noalloc(dims, **over):
+    lib = _lib()
+    a = dict(q=FAKE, k=FAKE + 1 * 4096, v=FAKE + 2 * 4096, g=None, bias=None, mask=None,
+             out=FAKE + 3 * 4096, lse=FAKE + 4 * 4096, dout=FAKE + 5 * 4096, dq=FAKE + 6 * 4096,
+             dk=FAKE + 7 * 4096, dv=FAKE + 8 * 4096, dg=None, dbias=None)
+    a.update(over)
+    P = lambda x: None if x is None else ctypes.c_void_p(x)
+    return lib.evo_attn_bwd_noalloc(ctypes.byref(dims), P(a["q"]), P(a["k"]), P(a["v"]), P(a["g"]),
+                                    P(a["bias"]), P(a["mask"]), P(a["out"]), P(a["lse"]), P(a["dout"]),
+                                    P(a["dq"]), P(a["dk"]), P(a["dv"]), P(a["dg"]), P(a["dbias"]), None)
+
+
+def test_noalloc_backward_validates_before_any_hip_call():
+    """The no-alloc backward checks its arguments like evo_attn_bwd and refuses
+    a problem whose scratch exceeds the fixed buffer with its own status, all
+    before any HIP call (nothing here touches a device)."""
+    lib = _lib()
+    limit = lib.evo_attn_bwd_noalloc_scratch_bytes()
+    assert limit == 64 << 20
+    d = _dims()
+    assert _bwd_noalloc(d, dq=None) == 1
+    assert _bwd_noalloc(d, g=FAKE + 9 * 4096) == 1                 # gate without dgate
+    assert _bwd_noalloc(d, dbias=FAKE + 10 * 4096) == 1            # dbias without bias
+    assert _bwd_noalloc(d, dv=FAKE + 8 * 4096 + 8) == 3
+    assert _bwd_noalloc(_dims(seq_len=300)) == 2
+    # 2048 rows x 256 keys x 8 heads x 32 channels: dA alone is 256 MiB
+    big = _dims(n_rows=2048, seq_len=256, n_heads=8, rows_per_bias=2048)
+    assert lib.evo_attn_bwd_workspace_size(ctypes.byref(big)) > limit
+    assert _bwd_noalloc(big) == 6
+    assert "no-alloc" in ea.evo_attn_strerror(6)
+    # empty problems: EVO_OK without any pointer
+    e = _dims(n_rows=0, rows_per_bias=1)
+    assert _bwd_noalloc(e, q=None, k=None, v=None, out=None, lse=None, dout=None, dq=None, dk=None,
+                        dv=None) == 0

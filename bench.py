@@ -43,6 +43,19 @@ def bias_transposed(w, es: int) -> bool:
     return bool(w.bias) and not (es == 2 and w.seq_len % 8 == 0)
 
 
+def fused_backward(w, es: int) -> bool:
+    """Whether the library runs the single-pass backward for this workload:
+    bf16 with head_dim <= 32; with a bias only where the chunk's dBias
+    accumulators fit (up to 128 keys, or head_dim 8 with rows of whole
+    16-byte groups)."""
+    if es != 2 or w.head_dim > 32:
+        return False
+    if not w.bias:
+        return True
+    nkt = (w.seq_len + 31) // 32
+    return nkt <= 4 or (w.head_dim == 8 and w.seq_len % 8 == 0)
+
+
 def kernel_model(w, es: int, ws_bytes: int):
     """Per-launch traffic and MFMA flops of every kernel of one step, in launch
     order, as (name, algorithmic bytes, workspace bytes, flops).
@@ -62,11 +75,22 @@ def kernel_model(w, es: int, ws_bytes: int):
     mask = N * L if w.mask != "none" else 0
     g = 1 if w.gate else 0
     S = N * H * L * L  # logits
+    fwd = ("fwd_kernel", (3 + g) * T + bias + mask + T + lse, 0, 4.0 * S * d)
+    if fused_backward(w, es):
+        # one pass: reads Q K V O dO [G] lse bias mask, writes dQ dK dV [dG]
+        # (and dBias itself when each plane is one row chunk); workspace:
+        # writes the partial dBias planes, which the reduction reads
+        parts = ws_bytes if w.bias else 0
+        ks = [fwd, ("bwd_fused_kernel", (5 + g) * T + lse + bias + mask + (3 + g) * T + (0 if parts else dbias),
+                    parts, 10.0 * S * d)]
+        if w.bias and parts:
+            ks.append(("dbias_tiles_reduce", dbias, parts, 0.0))
+        return ks
     transposed = bias_transposed(w, es)
     biast = bias if transposed else 0
     dsum = lse
     parts = max(0, ws_bytes - _align(T) - _align(dsum) - (_align(biast) if transposed else 0))
-    ks = [("fwd_kernel", (3 + g) * T + bias + mask + T + lse, 0, 4.0 * S * d)]
+    ks = [fwd]
     if transposed:
         ks.append(("bias_transpose", bias, biast, 0.0))
     # dK/dV pass: reads Q K V O dO [G] lse bias mask, writes dK dV [dG];
@@ -213,7 +237,10 @@ def main():
     fwd_ms = float(np.mean(fwd_warm))
     bwd_ms = float(np.mean(bwd_warm))
     kern_ms = [fwd_ms] + [float(np.mean([l_[j].elapsed_time(l_[j + 1]) for l_ in bev])) for j in range(nk)]
-    if w.bias and not bias_transposed(w, es):
+    model = kernel_model(w, es, ws.numel())
+    if fused_backward(w, es):
+        kern_ms = kern_ms[:len(model)]  # the slots after the last kernel bracket nothing
+    elif w.bias and not bias_transposed(w, es):
         del kern_ms[1]  # the transpose slot brackets no kernel
 
     # cold mode: a 512 MiB scratch buffer is written before every timed call
@@ -241,7 +268,6 @@ def main():
     flops = w.flops_fwd() + w.flops_bwd()
     tflops = flops / (ms_step * 1e-3) / 1e12
     fwd_bytes, bwd_bytes = algorithmic_bytes(w, es)
-    model = kernel_model(w, es, ws.numel())
     assert len(model) == len(kern_ms), (len(model), len(kern_ms))
     kernels = {}
     for (name, nbytes, wsb, kflops), ms in zip(model, kern_ms):

@@ -16,7 +16,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libevoattn.so")
 OBJDIR = os.path.join(PKG, "_build")
 
-SOURCES = ["evo_fwd.hip", "evo_bwd.hip", "evo_ln.hip", "evo_proj.hip", "evo_pair_bias.hip", "evo_optim.hip",
+SOURCES = ["evo_fwd.hip", "evo_bwd.hip", "evo_bwd_fused.hip", "evo_ln.hip", "evo_proj.hip", "evo_pair_bias.hip", "evo_optim.hip",
            "evo_proj_bwd.hip", "evo_pair_bias_bwd.hip",
            "evo_api.cpp", "evo_ln_api.cpp", "evo_proj_api.cpp", "evo_optim_api.cpp", "evo_graph.cpp"]
 

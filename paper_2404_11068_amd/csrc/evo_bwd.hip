@@ -122,35 +122,13 @@ struct KvArgs {
     float scale;
 };
 
-// bf16 pair bias of (query tile qt, key tile kt) as it lies in memory: lane
-// l holds the 16-byte chunks l and l + 64 of the 32 x 32 block (row = chunk
-// / 4 = query, 8 keys per chunk).  Rows past L read zeros.
-__device__ __forceinline__ void bias_block_load(rsrc_t rb, int L, int qt, int kt, int lane, u32x4 (&raw)[2]) {
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-        const int r = (lane >> 2) + 16 * j, cc = lane & 3;
-        const int qi = qt * 32 + r;
-        raw[j] = bload16(rb, qi < L ? (uint32_t)(qi * L + kt * 32 + 8 * cc) * 2u : kOOB);
-    }
-}
-
-// The block through this wave's own 32 x 32 LDS tile (no barrier: a wave's
-// LDS accesses complete in order): stored with column c holding key sig(c),
-// then read back with the transposing read, which hands lane n the column
-// sig(n), i.e. key n, at the query rows krow(i, h) of register i -- the
-// logit layout of the kv tile.
+// The bias block of (query tile qt, key tile kt) through this wave's own
+// LDS tile (bias_block_load / bias_block_transpose_raw in evo_frag.h), as
+// fp32 in the logit layout of the kv tile: lane n = key n, register i =
+// query krow(i, h).
 __device__ __forceinline__ void bias_block_transpose(uint16_t *tile, const u32x4 (&raw)[2], int lane,
                                                      float *out16) {
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-        const int r = (lane >> 2) + 16 * j, cc = lane & 3;
-        // keys 8cc + 4b + e (e < 4) go to column sig(8cc + 4b + e) = 16(cc/2) + 8b + 4(cc%2) + e
-        const int c0 = 16 * (cc >> 1) + 4 * (cc & 1);
-        const u32x2 lo = {raw[j].x, raw[j].y}, hi = {raw[j].z, raw[j].w};
-        *reinterpret_cast<u32x2 *>(&tile[r * 32 + c0]) = lo;
-        *reinterpret_cast<u32x2 *>(&tile[r * 32 + c0 + 8]) = hi;
-    }
-    const Tr<bf16_t>::K32 f = load_k32_tr(tile, 32, 0, 32, lane);
+    const Tr<bf16_t>::K32 f = bias_block_transpose_raw(tile, raw, lane);
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
         const u32x4 w = __builtin_bit_cast(u32x4, f.v[t]);
@@ -830,6 +808,27 @@ hipError_t launch_bwd_t(const Problem &p, const BwdPtrs &x, void *ws, const BwdP
 }  // namespace
 
 BwdPlan plan_bwd(const Problem &p, bool has_bias, size_t cap) {
+    if (fused_bwd_supported(p, has_bias)) {
+        // single pass: the workspace holds the partial dBias planes only;
+        // with a cap, fewer row chunks (fewer planes) until it fits
+        BwdPlan pl{};
+        pl.fused = true;
+        int64_t chunks = 1, g = 1;
+        fused_bwd_chunks(p, has_bias, &chunks, &g);
+        const int64_t rpb = has_bias ? p.rpb : 1;
+        size_t total = has_bias ? fused_bwd_partial_bytes(p, chunks) : 0;
+        while (total > cap && chunks > 1) {
+            const int64_t fewer = chunks / 2 < chunks - 1 ? chunks / 2 : chunks - 1;
+            g = (rpb + fewer - 1) / fewer;
+            chunks = (rpb + g - 1) / g;
+            total = fused_bwd_partial_bytes(p, chunks);
+        }
+        pl.chunks = chunks;
+        pl.rows_per_chunk = g;
+        pl.off_part = 0;
+        pl.total = total;
+        return pl;
+    }
     const int64_t es = p.dtype == 1 ? 2 : 4;
     const int64_t planes = has_bias ? p.N / p.rpb : (p.N > 0 ? 1 : 0);
     const int64_t rpb = has_bias ? p.rpb : p.N;
@@ -855,7 +854,8 @@ BwdPlan plan_bwd(const Problem &p, bool has_bias, size_t cap) {
     // workspace layout for a given number of row chunks; with a cap, fewer
     // chunks (fewer partial dBias planes, longer qbias workgroups) until it fits
     auto layout = [&](int64_t want) {
-        BwdPlan pl;
+        BwdPlan pl{};
+        pl.fused = false;
         int64_t g = 1, c = 0;
         if (want > 0) {
             g = (rpb + want - 1) / want;
@@ -923,8 +923,17 @@ hipError_t launch_bwd(const Problem &p, const BwdPtrs &x, void *ws, const BwdPla
                       Tracer *tr) {
     Tracer none;
     Tracer &t = tr ? *tr : none;
-    if (p.dtype == 1) return launch_bwd_t<bf16_t>(p, x, ws, plan, s, t);
-    return launch_bwd_t<float>(p, x, ws, plan, s, t);
+    hipError_t e;
+    if (plan.fused) {
+        t.mark(s);
+        e = launch_bwd_fused(p, x, ws, plan.chunks, plan.rows_per_chunk, s, t);
+    } else if (p.dtype == 1) {
+        e = launch_bwd_t<bf16_t>(p, x, ws, plan, s, t);
+    } else {
+        e = launch_bwd_t<float>(p, x, ws, plan, s, t);
+    }
+    if (e == hipSuccess) t.fill(s);
+    return e;
 }
 
 }  // namespace evo

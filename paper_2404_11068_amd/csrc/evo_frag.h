@@ -312,6 +312,43 @@ __device__ __forceinline__ Tr<bf16_t>::K32 load_k32_tr_sw32(const uint16_t *X, i
 }
 
 // ---------------------------------------------------------------------------
+// A 32 x 32 block of a bf16 pair-bias plane [query][key] (row length L, a
+// multiple of 8 so that every 16-byte group lies inside one row), handed to
+// the lanes that own keys.
+//
+// bias_block_load: lane l reads the 16-byte chunks l and l + 64 of the block
+// of (query tile qt, key tile kt) as it lies in memory (row = chunk / 4 =
+// query, 8 keys per chunk).  Rows past L read zeros.
+__device__ __forceinline__ void bias_block_load(rsrc_t rb, int L, int qt, int kt, int lane, u32x4 (&raw)[2]) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int r = (lane >> 2) + 16 * j, cc = lane & 3;
+        const int qi = qt * 32 + r;
+        raw[j] = bload16(rb, qi < L ? (uint32_t)(qi * L + kt * 32 + 8 * cc) * 2u : kOOB);
+    }
+}
+
+// bias_block_transpose_raw: the block through a wave's own 32 x 32 LDS tile
+// (no barrier: a wave's LDS accesses complete in order), stored with column c
+// holding key sig(c) and read back with the transposing read, which hands
+// lane n the column sig(n), i.e. key n, at the query rows krow(i, h) of
+// register i (packed bf16 in the k32 order) -- the logit layout of a tile
+// whose lanes own keys.
+__device__ __forceinline__ Tr<bf16_t>::K32 bias_block_transpose_raw(uint16_t *tile, const u32x4 (&raw)[2],
+                                                                    int lane) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int r = (lane >> 2) + 16 * j, cc = lane & 3;
+        // keys 8cc + 4b + e (e < 4) go to column sig(8cc + 4b + e) = 16(cc/2) + 8b + 4(cc%2) + e
+        const int c0 = 16 * (cc >> 1) + 4 * (cc & 1);
+        const u32x2 lo = {raw[j].x, raw[j].y}, hi = {raw[j].z, raw[j].w};
+        *reinterpret_cast<u32x2 *>(&tile[r * 32 + c0]) = lo;
+        *reinterpret_cast<u32x2 *>(&tile[r * 32 + c0 + 8]) = hi;
+    }
+    return load_k32_tr(tile, 32, 0, 32, lane);
+}
+
+// ---------------------------------------------------------------------------
 // Constant A operand "c times a permuted identity" for the k32 contraction:
 // A[m][k] = c where k-slot k holds row sig(m) of the tile, else 0.  With a B
 // operand holding X[k][n] (k = key row of the tile, n = query), the product

@@ -32,11 +32,17 @@ struct BwdPtrs {
     float *dbias;
 };
 
-// Backward scratch plan: where each buffer lives inside the workspace.
+// Backward scratch plan: which kernels run and where each buffer lives
+// inside the workspace.
+//   fused (bf16, head_dim <= 32): one pass; the workspace holds only the
+//     partial dBias planes (chunks > 1), at offset 0
+//   otherwise: the dK/dV pass and the dQ/dBias pass, with dA, Dsum, the
+//     transposed bias and the partial dBias planes in the workspace
 struct BwdPlan {
+    bool fused;
     int64_t chunks;          // row chunks per bias plane (dBias partial planes per plane and head)
-    int64_t rows_per_chunk;  // rows handled by one qbias workgroup
-    int64_t n_wg;            // workgroups of the qbias kernel
+    int64_t rows_per_chunk;  // rows handled by one workgroup of the dBias-producing pass
+    int64_t n_wg;            // workgroups of the qbias kernel (two-pass plan)
     size_t off_da, off_dsum, off_biast, off_part, total;
 };
 
@@ -60,7 +66,18 @@ struct Tracer {
         if (ev && next < n) (void)hipEventRecord(ev[next], s);
         ++next;
     }
+    // record the events no kernel claimed (they bracket nothing)
+    void fill(hipStream_t s) {
+        while (ev && next < n) mark(s);
+    }
 };
+
+// single-pass backward (evo_bwd_fused.hip)
+bool fused_bwd_supported(const Problem &p, bool has_bias);
+void fused_bwd_chunks(const Problem &p, bool has_bias, int64_t *chunks, int64_t *rows_per_chunk);
+size_t fused_bwd_partial_bytes(const Problem &p, int64_t chunks);
+hipError_t launch_bwd_fused(const Problem &p, const BwdPtrs &x, void *ws, int64_t chunks, int64_t rows_per_chunk,
+                            hipStream_t s, Tracer &tr);
 
 // kernels launched by one backward call (for Tracer sizing)
 int bwd_kernel_count(bool has_bias);

@@ -112,11 +112,17 @@ def test_bwd_rejects_invalid_calls():
     assert _bwd(d, dq=None) == 1
     assert _bwd(d, g=FAKE + 9 * 4096) == 1                 # gate without dgate
     assert _bwd(d, dbias=FAKE + 10 * 4096) == 1            # dbias without bias
-    assert _bwd(d, ws=None) == 4
-    assert _bwd(d, ws_bytes=16) == 4
-    assert _bwd(d, ws=FAKE + (1 << 20) + 16) == 4          # workspace not 256-byte aligned
     assert _bwd(d, dv=FAKE + 8 * 4096 + 8) == 3
     assert _bwd(_dims(seq_len=300)) == 2
+    # workspace checks, on plans that need scratch: fp32 (two passes, dA and
+    # Dsum in the workspace) and bf16 with a bias over many rows (partial
+    # dBias planes of the single pass)
+    bias = dict(bias=FAKE + 9 * 4096, dbias=FAKE + 10 * 4096)
+    for dd, extra in ((_dims(dtype=0), {}), (_dims(n_rows=64, seq_len=64, rows_per_bias=64), bias)):
+        assert _lib().evo_attn_bwd_workspace_size(ctypes.byref(dd)) > 256
+        assert _bwd(dd, ws=None, **extra) == 4
+        assert _bwd(dd, ws_bytes=16, **extra) == 4
+        assert _bwd(dd, ws=FAKE + (1 << 20) + 16, **extra) == 4      # workspace not 256-byte aligned
 
 
 def test_traced_backward_validates_events():
@@ -185,8 +191,9 @@ def test_noalloc_backward_validates_before_any_hip_call():
     assert _bwd_noalloc(d, dbias=FAKE + 10 * 4096) == 1            # dbias without bias
     assert _bwd_noalloc(d, dv=FAKE + 8 * 4096 + 8) == 3
     assert _bwd_noalloc(_dims(seq_len=300)) == 2
-    # 2048 rows x 256 keys x 8 heads x 32 channels: dA alone is 256 MiB
-    big = _dims(n_rows=2048, seq_len=256, n_heads=8, rows_per_bias=2048)
+    # fp32, 2048 rows x 128 keys x 8 heads x 32 channels: the two-pass plan's
+    # dA alone is 256 MiB
+    big = _dims(dtype=0, n_rows=2048, seq_len=128, n_heads=8, rows_per_bias=2048)
     assert lib.evo_attn_bwd_workspace_size(ctypes.byref(big)) > limit
     assert _bwd_noalloc(big) == 6
     assert "no-alloc" in ea.evo_attn_strerror(6)

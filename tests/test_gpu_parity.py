@@ -55,6 +55,15 @@ SMALL = [
     (3, 64, 2, 64, "bf16", dict(gate=False, bias=False, mask="none")),
     (2, 96, 1, 64, "f32", dict()),
     (2, 128, 2, 64, "f32", dict(rpb=1, mask="tail_pad")),
+    # single-pass backward (bf16, head_dim <= 32; with a bias up to 128 keys, or
+    # head_dim 8 at 256): several rows per chunk with partial dBias planes and
+    # their reduction, one chunk per plane (dBias written directly), no bias
+    (96, 256, 8, 8, "bf16", dict()),
+    (128, 128, 8, 32, "bf16", dict(rpb=16, mask="length")),
+    (64, 96, 2, 16, "bf16", dict(p=0.2)),
+    (3, 200, 2, 8, "bf16", dict(rpb=1)),
+    (5, 256, 3, 8, "bf16", dict(bias=False, gate=False)),
+    (4, 256, 2, 32, "bf16", dict(bias=False, mask="length")),
 ]
 
 
@@ -175,10 +184,12 @@ def test_empty_problems_are_noops():
         assert out.numel() == 0 and dq.numel() == 0
 
 
-def test_backward_is_bitwise_repeatable_and_stream_ordered():
+@pytest.mark.parametrize("name,rows", [("msa_row_bias_bf16", 16), ("extra_msa_bf16", 64)])
+def test_backward_is_bitwise_repeatable_and_stream_ordered(name, rows):
     """Two calls on a non-default stream give identical bits: every sum in the
-    backward (over keys, queries and rows) runs in a fixed order."""
-    w = W.by_name("msa_row_bias_bf16").with_rows(16)
+    backward (over keys, queries and rows) runs in a fixed order (two-pass
+    backward at head_dim 32 with 256 keys, single pass at head_dim 8)."""
+    w = W.by_name(name).with_rows(rows)
     x = W.generate(w)
     s = torch.cuda.Stream()
     with torch.cuda.stream(s):

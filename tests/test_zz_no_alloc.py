@@ -81,11 +81,11 @@ def test_noalloc_fp32_and_no_bias():
 
 
 def test_noalloc_refuses_what_does_not_fit():
-    """2048 rows x 256 keys x 8 heads x 32 channels: the per-row scratch alone
-    is past the fixed buffer; the call is refused before any work is queued
-    and the outputs are untouched."""
-    N, L, H, d = 2048, 256, 8, 32
-    q = torch.zeros((N, L, H, d), dtype=torch.bfloat16, device="cuda")
+    """fp32, 2048 rows x 128 keys x 8 heads x 32 channels: the per-row scratch
+    of the two-pass backward (dA, 256 MiB) is past the fixed buffer; the call
+    is refused before any work is queued and the outputs are untouched."""
+    N, L, H, d = 2048, 128, 8, 32
+    q = torch.zeros((N, L, H, d), dtype=torch.float32, device="cuda")
     lse = torch.zeros((N, H, L), dtype=torch.float32, device="cuda")
     dq = torch.full_like(q, 3.0)
     with pytest.raises(ea.EvoAttnError) as e:

@@ -87,6 +87,37 @@ __device__ __forceinline__ Tr<bf16_t>::K32 ds_transpose(uint16_t *tile, const Tr
 template <int NKT, int NQR>
 constexpr int kLdsBiasTiles = NKT > NQR ? NKT - NQR : 0;
 
+// The pair bias of (query tile qt, key tile kt) as the A operand of a k32
+// product: lane m takes the bias row of query qt*32 + sig(m) (the permuted
+// rows of the Q operand of S = Q K^T), k-slots = keys kt*32 + {8h+s, 16+8h+s},
+// as it lies in memory.  Times sqrt(d) on an identity B operand it adds
+// sqrt(d) * bias to the logit tile whose lanes own keys.  BV: rows of whole
+// 16-byte groups (two loads per lane); otherwise one element per load.  Rows
+// and keys past L read zeros.
+template <bool BV>
+__device__ __forceinline__ Tr<bf16_t>::K32 bias_rows_k32(rsrc_t rb, int L, int qt, int kt, int lane) {
+    const int m = lane & 31, h = lane >> 5;
+    const int qi = qt * 32 + sig(m);
+    const int k0 = kt * 32 + 8 * h;
+    Tr<bf16_t>::K32 f;
+    if constexpr (BV) {
+        f.v[0] = __builtin_bit_cast(bf16x8, bload16(rb, qi < L ? (uint32_t)(qi * L + k0) * 2u : kOOB));
+        f.v[1] = __builtin_bit_cast(bf16x8, bload16(rb, qi < L ? (uint32_t)(qi * L + k0 + 16) * 2u : kOOB));
+    } else {
+        short8tr w[2];
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int kj = k0 + 16 * t + e;
+                w[t][e] = (short)bload2(rb, (qi < L && kj < L) ? (uint32_t)(qi * L + kj) * 2u : kOOB);
+            }
+        f.v[0] = __builtin_bit_cast(bf16x8, w[0]);
+        f.v[1] = __builtin_bit_cast(bf16x8, w[1]);
+    }
+    return f;
+}
+
 template <int D, int NKT, bool HB, bool BV, int NQR>
 __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
     using E = uint16_t;
@@ -137,6 +168,16 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
     const rsrc_t rb = HB ? make_buf((const E *)a.bias + (b * a.H + hh) * (int64_t)L * L, (uint32_t)(L * L * ES))
                          : none;
     uint16_t *const tp = &tp_lds[wave * 1024];
+    // sqrt(d) on an identity, for the bias product (two bf16 terms where
+    // sqrt(d) has no exact bf16 value; their sum matches it to ~3e-7)
+    float sq_hi, sq_lo;
+    sqrt_split(D, sq_hi, sq_lo);
+    const bool two_term = sq_lo != 0.0f;
+    K32 eye_hi{}, eye_lo{};
+    if constexpr (HB) {
+        eye_hi = eye_k32(sq_hi, lane);
+        if (two_term) eye_lo = eye_k32(sq_lo, lane);
+    }
 
     // dS of this wave's keys summed over the rows of the chunk, per query
     // tile: tiles below NQR in registers, the rest in the wave's LDS region
@@ -179,9 +220,9 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
                 gv[j] = bload16(rg, off);
             }
         }
-        // first query tile's bias block
-        u32x4 braw[2];
-        if constexpr (HB && BV) bias_block_load(rb, L, 0, kt, lane, braw);
+        // first query tile's bias rows
+        K32 bnext;
+        if constexpr (HB) bnext = bias_rows_k32<BV>(rb, L, 0, kt, lane);
 
         // ---- staging: Q and dA into LDS; dA, Dsum and dG from dO, O and G
         {
@@ -232,6 +273,7 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
         const bool kvalid = kin && (!has_mask || mbyte != 0);
         const uint64_t kbal = __ballot(kvalid);
         const bool kfull = kbal == ~0ull, kany = kbal != 0ull;
+        const short mask_neg = kvalid ? (short)0 : kBf16MaskNeg;  // rank-1 term on this lane's key column
         __syncthreads();
 
         f32x16 dv_acc = zero16(), dk_acc = zero16();
@@ -240,32 +282,30 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
         for (int qt = 0; qt < NKT; ++qt) {
             if (qt >= nqt) break;
             float *const dq_part = dqp[qt & 1];
-            // the next tile's bias block goes out first (loads complete in order)
+            // the next tile's bias rows go out first (loads complete in order)
             K32 bcur;
-            if constexpr (HB && BV) {
-                bcur = bias_block_transpose_raw(tp, braw, lane);
-                if (qt + 1 < NKT) bias_block_load(rb, L, qt + 1, kt, lane, braw);
-            } else if constexpr (HB) {
-                // rows not made of whole 16-byte groups: one element per load
-                short8tr w[2];
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int qi = qt * 32 + krow(i, h2);
-                    w[i >> 3][i & 7] = (short)bload2(rb, (qi < L && kin) ? (uint32_t)(qi * L + key) * 2u : kOOB);
-                }
-                bcur.v[0] = __builtin_bit_cast(bf16x8, w[0]);
-                bcur.v[1] = __builtin_bit_cast(bf16x8, w[1]);
+            if constexpr (HB) {
+                bcur = bnext;
+                if (qt + 1 < NKT) bnext = bias_rows_k32<BV>(rb, L, qt + 1, kt, lane);
             }
             f32x16 dq = zero16();
             if (kany) {
-                // S = Q K^T and dP = dA V^T for 32 queries x this wave's 32
-                // keys; lane = key, reg i = query qt*32 + krow(i, h2)
+                // raw logits S = Q K^T + sqrt(d) * bias (bias through the
+                // matrix unit, sqrt(d) as one or two bf16 terms; masked keys
+                // get -2^64 from a rank-1 term) and dP = dA V^T, for 32
+                // queries x this wave's 32 keys; lane = key, reg i = query
+                // qt*32 + krow(i, h2)
                 f32x16 S = zero16(), dP = zero16();
                 {
                     ChFrag<bf16_t, D> qa, daa;
                     qa.load(&q_lds[(qt * 32 + sig(n)) * RSTR], h2);
                     daa.load(&da_lds[(qt * 32 + sig(n)) * RSTR], h2);
                     ChFrag<bf16_t, D>::mma(S, qa, kb);
+                    if constexpr (HB) {
+                        Tr<bf16_t>::mma_k32(S, bcur, eye_hi);
+                        if (two_term) Tr<bf16_t>::mma_k32(S, bcur, eye_lo);
+                    }
+                    if (!kfull) mma_rank1(S, kBf16One, mask_neg, h2);
                     ChFrag<bf16_t, D>::mma(dP, daa, vb);
                 }
                 f32x16 P, dS;
@@ -277,25 +317,12 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
                     const f32x4 l0 = lp[0], l1 = lp[1], d0 = dp[0], d1 = dp[1];
                     const float l2[8] = {l0.x, l0.y, l0.z, l0.w, l1.x, l1.y, l1.z, l1.w};
                     const float ds[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
-                    float bb[8];
-                    if constexpr (HB) {
-                        const u32x4 w = __builtin_bit_cast(u32x4, bcur.v[half]);
-                        const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-                        for (int s2 = 0; s2 < 4; ++s2) {
-                            bb[2 * s2] = __builtin_bit_cast(float, ws[s2] << 16);
-                            bb[2 * s2 + 1] = __builtin_bit_cast(float, ws[s2] & 0xffff0000u);
-                        }
-                    }
 #pragma unroll
                     for (int s8 = 0; s8 < 8; ++s8) {
                         const int i = 8 * half + s8;
-                        // log2 P = c2 * S + log2(e) * bias - lse * log2(e)
-                        const float x = HB ? __builtin_fmaf(bb[s8], kLog2e, -l2[s8]) : -l2[s8];
-                        float p = __builtin_amdgcn_exp2f(__builtin_fmaf(S[i], c2, x));
-                        // masked key: P is exactly 0 (a select: a masked
-                        // logit far above the lse gives exp2 = +inf)
-                        if (!kfull) p = kvalid ? p : 0.0f;
+                        // log2 P = c2 * S_raw - lse * log2(e); a masked key's
+                        // S_raw is below -2^63, so its P is exactly 0
+                        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(S[i], c2, -l2[s8]));
                         P[i] = p;
                         dS[i] = p * (dP[i] - ds[s8]);
                     }
@@ -318,15 +345,17 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
                 const K32 dsb = Tr<bf16_t>::pack(dS);
                 // dV^T += dA^T P ;  dK^T += Q^T dS   (A rows: channel sig(n))
                 {
-                    const K32 dat = load_k32_tr(da_lds, RSTR, qt * 32, D, lane);
+                    // (operand rows of channels >= D only reach output
+                    // rows that are never stored: no zeroing needed)
+                    const K32 dat = load_k32_tr(da_lds, RSTR, qt * 32, D, lane, false, false);
                     Tr<bf16_t>::mma_k32(dv_acc, dat, pb);
-                    const K32 qtf = load_k32_tr(q_lds, RSTR, qt * 32, D, lane);
+                    const K32 qtf = load_k32_tr(q_lds, RSTR, qt * 32, D, lane, false, false);
                     Tr<bf16_t>::mma_k32(dk_acc, qtf, dsb);
                 }
                 // dQ^T share of this key tile = K^T dS^T (lane = query n, reg
                 // i = channel krow(i, h2))
                 const K32 dsT = ds_transpose(tp, dsb, n, h2);
-                const K32 kT = load_k32_tr(k_lds, RSTR, kt * 32, D, lane);
+                const K32 kT = load_k32_tr(k_lds, RSTR, kt * 32, D, lane, false, false);
                 Tr<bf16_t>::mma_k32(dq, kT, dsT);
             }
             // ---- this wave's dQ share into LDS; fixed-order sum over the waves
@@ -342,9 +371,11 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
                 }
             }
             __syncthreads();
+            // the sum of tile qt is taken by the threads from wave qt % NKT on
+            const int rot = (tid + NT - (qt % NKT) * 64) % NT;
 #pragma unroll
             for (int j = 0; j < NSUM; ++j) {  // four consecutive channels per thread and step
-                const int idx = tid + j * NT;
+                const int idx = rot + j * NT;
                 const int q = idx / (D / 4), cq = idx % (D / 4);
                 const bool ok = idx < 32 * (D / 4);
                 f32x4 sum = {0.0f, 0.0f, 0.0f, 0.0f};

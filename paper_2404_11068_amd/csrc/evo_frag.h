@@ -242,8 +242,11 @@ template <> struct ChFrag<bf16_t, 8> {
 typedef short short4tr __attribute__((ext_vector_type(4)));
 typedef short short8tr __attribute__((ext_vector_type(8)));
 
+// With zero_cols false the lanes whose operand row is a channel >= ncols keep
+// what the read gave them (finite data of the tile): enough wherever those
+// rows only feed output rows that are never stored.
 __device__ __forceinline__ Tr<bf16_t>::K32 load_k32_tr(const uint16_t *X, int stride, int kbase, int ncols,
-                                                      int lane, bool ones_row = false) {
+                                                      int lane, bool ones_row = false, bool zero_cols = true) {
     const int G = lane >> 4, i = lane & 15;
     const int q = i & 3;
     int c0 = 16 * (G & 1) + 4 * (((q & 1) << 1) | (q >> 1));
@@ -265,7 +268,7 @@ __device__ __forceinline__ Tr<bf16_t>::K32 load_k32_tr(const uint16_t *X, int st
     // the operand row of this lane is channel sig(lane % 32); with ones_row,
     // channel ncols (< 32) is all ones, so the product also yields column sums
     const int ch = sig(lane & 31);
-    if (ch >= ncols) {
+    if (zero_cols && ch >= ncols) {
         const short v = (ones_row && ch == ncols) ? (short)0x3F80 : (short)0;
         const short8tr w = {v, v, v, v, v, v, v, v};
         f.v[0] = __builtin_bit_cast(bf16x8, w);
@@ -363,6 +366,21 @@ __device__ __forceinline__ Tr<bf16_t>::K32 diag_k32(float c, int lane) {
     for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int s = 0; s < 8; ++s) f.v[t][s] = (__bf16)((r == 16 * t + 8 * h + s) ? c : 0.0f);
+    return f;
+}
+
+// Constant B operand "c times the identity" for the k32 contraction:
+// B[k][n] = c where k == n.  With an A operand holding X[m][k] (k = key of
+// the tile, rows in any order), the product adds c * X[m][n] to the tile --
+// a [query][key] block read along keys lands in a logit tile whose lanes own
+// keys.
+__device__ __forceinline__ Tr<bf16_t>::K32 eye_k32(float c, int lane) {
+    const int n = lane & 31, h = lane >> 5;
+    Tr<bf16_t>::K32 f;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int s = 0; s < 8; ++s) f.v[t][s] = (__bf16)((16 * t + 8 * h + s == n) ? c : 0.0f);
     return f;
 }
 

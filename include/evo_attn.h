@@ -73,8 +73,11 @@ enum evo_attn_status {
 };
 
 /* Compiled limits: head_dim in {8, 16, 32, 64}; 0 <= seq_len <= EVO_ATTN_MAX_SEQ_LEN
- * (fp32 with head_dim 64: seq_len <= EVO_ATTN_MAX_SEQ_LEN_F32_D64, the most the
- * backward's LDS tiles hold).  Head dims 8, 16 and 32 cover every Evoformer
+ * (512) for bf16 with head_dim <= 32; seq_len <= EVO_ATTN_MAX_SEQ_LEN_WIDE (256)
+ * for fp32 and for head_dim 64; fp32 with head_dim 64: seq_len <=
+ * EVO_ATTN_MAX_SEQ_LEN_F32_D64 (128).  Each bound is the most keys whose
+ * staged tiles the kernels hold in a workgroup's LDS (a row of 257..512 keys
+ * runs as 16-wave workgroups).  Head dims 8, 16 and 32 cover every Evoformer
  * attention (MSA row and column, triangle, extra-MSA); head_dim 64 runs each
  * (row, head) as two workgroups that form the same logits from all 64 channels
  * and produce 32 output channels each.
@@ -86,7 +89,8 @@ enum evo_attn_status {
  * the gradients stay within 2e-2 abs + 2e-2 rel of the exact ones on such
  * inputs; at head_dim 64 a strongly peaked softmax (logit gaps of tens) can put
  * single dBias elements a few percent past that bound. */
-#define EVO_ATTN_MAX_SEQ_LEN 256
+#define EVO_ATTN_MAX_SEQ_LEN 512
+#define EVO_ATTN_MAX_SEQ_LEN_WIDE 256     /* fp32, or head_dim 64 */
 #define EVO_ATTN_MAX_SEQ_LEN_F32_D64 128
 
 typedef struct evo_attn_dims {

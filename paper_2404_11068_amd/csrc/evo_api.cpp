@@ -21,6 +21,8 @@ int check_dims(const evo_attn_dims *d, bool has_bias, evo::Problem *p) {
     if (d->n_heads < 1 || d->head_dim < 1 || d->n_rows < 0 || d->seq_len < 0) return EVO_ERR_INVALID_ARG;
     if (d->head_dim != 8 && d->head_dim != 16 && d->head_dim != 32 && d->head_dim != 64) return EVO_ERR_UNSUPPORTED;
     if (d->seq_len > EVO_ATTN_MAX_SEQ_LEN) return EVO_ERR_UNSUPPORTED;
+    if ((d->dtype == EVO_DTYPE_F32 || d->head_dim == 64) && d->seq_len > EVO_ATTN_MAX_SEQ_LEN_WIDE)
+        return EVO_ERR_UNSUPPORTED;
     // fp32 at head_dim 64: the backward's LDS tiles fit up to 128 keys
     if (d->dtype == EVO_DTYPE_F32 && d->head_dim == 64 && d->seq_len > EVO_ATTN_MAX_SEQ_LEN_F32_D64)
         return EVO_ERR_UNSUPPORTED;

@@ -745,8 +745,14 @@ hipError_t launch_passes_d(const Problem &p, const KvArgs &ka, const QbArgs &qa,
     if (nkt <= 4) return launch_passes_v<T, D, 4>(p, ka, qa, s, tr);
     // fp32 at head_dim 64 past 128 keys would need more than the 160 KB of LDS
     // (the ABI rejects it before this point)
-    if constexpr (sizeof(typename Tr<T>::elem) == 4 && D > 32) return hipErrorInvalidValue;
-    else return launch_passes_v<T, D, 8>(p, ka, qa, s, tr);
+    if (nkt <= 8) {
+        if constexpr (sizeof(typename Tr<T>::elem) == 4 && D > 32) return hipErrorInvalidValue;
+        else return launch_passes_v<T, D, 8>(p, ka, qa, s, tr);
+    }
+    // 257..512 keys: 16-wave workgroups, bf16 with head_dim <= 32 only (the
+    // staged Q and dA of 512 tokens fill the LDS otherwise)
+    if constexpr (sizeof(typename Tr<T>::elem) == 2 && D <= 32) return launch_passes_v<T, D, 16>(p, ka, qa, s, tr);
+    else return hipErrorInvalidValue;
 }
 
 template <typename T>
@@ -833,7 +839,7 @@ BwdPlan plan_bwd(const Problem &p, bool has_bias, size_t cap) {
     const int64_t planes = has_bias ? p.N / p.rpb : (p.N > 0 ? 1 : 0);
     const int64_t rpb = has_bias ? p.rpb : p.N;
     const int64_t nqt = (p.L + 31) / 32;
-    const int64_t waves = nqt <= 1 ? 1 : nqt <= 2 ? 2 : nqt <= 4 ? 4 : 8;  // per qbias workgroup
+    const int64_t waves = nqt <= 1 ? 1 : nqt <= 2 ? 2 : nqt <= 4 ? 4 : nqt <= 8 ? 8 : 16;  // per qbias workgroup
     // qbias workgroups: enough waves to fill the chip twice over (4096 = two
     // 8-wave workgroups on each of 256 CUs: the kernel's registers and LDS
     // allow two per CU), with as few row chunks as that allows (each chunk

@@ -572,9 +572,9 @@ hipError_t launch_fused_d(const Problem &p, const FusedArgs &fa, hipStream_t s) 
 }  // namespace
 
 bool fused_bwd_supported(const Problem &p, bool has_bias) {
-    if (p.dtype != 1 || p.D > 32) return false;
-    if (!has_bias) return true;
     const int64_t nkt = (p.L + 31) / 32;
+    if (p.dtype != 1 || p.D > 32 || nkt > 8) return false;  // (its LDS tiles hold up to 256 keys)
+    if (!has_bias) return true;
     return nkt <= 4 || (p.D == 8 && p.L % 8 == 0);
 }
 

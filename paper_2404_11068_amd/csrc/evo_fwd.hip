@@ -5,7 +5,7 @@
 // pair bias enters the logits before the softmax; all of MHA in one kernel).
 //
 // Work unit = one (row, head), one workgroup per unit, one wave per
-// 32-query tile (seq_len <= 256, so at most 8 waves); at head_dim 64 a unit
+// 32-query tile (at most 16 waves: 512 keys); at head_dim 64 a unit
 // is a (row, head, half of the channels of O): both halves form the same
 // logits from all 64 channels, each produces 32 channels of O, and the first
 // writes the log-sum-exp.  The kernel keeps its
@@ -427,7 +427,11 @@ hipError_t launch_d(const Problem &p, const FwdPtrs &x, hipStream_t s) {
     if (nkt <= 1) return launch_t<T, D, 1>(p, x, s);
     if (nkt <= 2) return launch_t<T, D, 2>(p, x, s);
     if (nkt <= 4) return launch_t<T, D, 4>(p, x, s);
-    return launch_t<T, D, 8>(p, x, s);
+    if (nkt <= 8) return launch_t<T, D, 8>(p, x, s);
+    // 257..512 keys: 16 query tiles, 16 waves (bf16, head_dim <= 32: K and V
+    // of 512 keys fit the LDS; the ABI rejects the rest before this point)
+    if constexpr (sizeof(typename Tr<T>::elem) == 2 && D <= 32) return launch_t<T, D, 16>(p, x, s);
+    else return hipErrorInvalidValue;
 }
 
 template <typename T>

@@ -27,7 +27,8 @@ LIB_PATH = os.path.join(_PKG, "libevoattn.so")
 
 EVO_DTYPE_F32 = 0
 EVO_DTYPE_BF16 = 1
-EVO_ATTN_MAX_SEQ_LEN = 256
+EVO_ATTN_MAX_SEQ_LEN = 512       # bf16, head_dim <= 32
+EVO_ATTN_MAX_SEQ_LEN_WIDE = 256  # fp32, or head_dim 64
 
 _DTYPES = {torch.float32: EVO_DTYPE_F32, torch.bfloat16: EVO_DTYPE_BF16}
 

@@ -65,7 +65,9 @@ def _fwd(dims, q=FAKE, k=FAKE + 4096, v=FAKE + 8192, g=None, bias=None, mask=Non
     (dict(head_dim=24), 2),
     (dict(head_dim=128), 2),
     (dict(dtype=0, head_dim=64, seq_len=129), 2),   # fp32 d=64: at most 128 keys
-    (dict(seq_len=257), 2),
+    (dict(seq_len=513), 2),
+    (dict(dtype=0, seq_len=257), 2),                # fp32: at most 256 keys
+    (dict(head_dim=64, seq_len=257), 2),            # head_dim 64: at most 256 keys
     (dict(n_heads=0), 1),
     (dict(n_rows=-1), 1),
     (dict(seq_len=-3), 1),
@@ -113,7 +115,7 @@ def test_bwd_rejects_invalid_calls():
     assert _bwd(d, g=FAKE + 9 * 4096) == 1                 # gate without dgate
     assert _bwd(d, dbias=FAKE + 10 * 4096) == 1            # dbias without bias
     assert _bwd(d, dv=FAKE + 8 * 4096 + 8) == 3
-    assert _bwd(_dims(seq_len=300)) == 2
+    assert _bwd(_dims(seq_len=520)) == 2
     # workspace checks, on plans that need scratch: fp32 (two passes, dA and
     # Dsum in the workspace) and bf16 with a bias over many rows (partial
     # dBias planes of the single pass)
@@ -190,7 +192,7 @@ def test_noalloc_backward_validates_before_any_hip_call():
     assert _bwd_noalloc(d, g=FAKE + 9 * 4096) == 1                 # gate without dgate
     assert _bwd_noalloc(d, dbias=FAKE + 10 * 4096) == 1            # dbias without bias
     assert _bwd_noalloc(d, dv=FAKE + 8 * 4096 + 8) == 3
-    assert _bwd_noalloc(_dims(seq_len=300)) == 2
+    assert _bwd_noalloc(_dims(seq_len=520)) == 2
     # fp32, 2048 rows x 128 keys x 8 heads x 32 channels: the two-pass plan's
     # dA alone is 256 MiB
     big = _dims(dtype=0, n_rows=2048, seq_len=128, n_heads=8, rows_per_bias=2048)

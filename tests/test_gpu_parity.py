@@ -64,6 +64,12 @@ SMALL = [
     (3, 200, 2, 8, "bf16", dict(rpb=1)),
     (5, 256, 3, 8, "bf16", dict(bias=False, gate=False)),
     (4, 256, 2, 32, "bf16", dict(bias=False, mask="length")),
+    # 257..512 keys (bf16, head_dim <= 32): 16-wave workgroups, two-pass backward
+    (3, 384, 2, 32, "bf16", dict()),
+    (2, 512, 2, 32, "bf16", dict(mask="length")),
+    (3, 512, 2, 8, "bf16", dict(p=0.2)),
+    (2, 333, 3, 16, "bf16", dict(rpb=1)),
+    (2, 460, 2, 8, "bf16", dict(bias=False, mask="tail_pad")),
 ]
 
 
@@ -108,14 +114,15 @@ _D64_RAMP = pytest.mark.xfail(reason="bf16 head_dim 64: D is formed from the bf1
                               strict=False)
 
 
-@pytest.mark.parametrize("dtype,d", [("bf16", 32), ("bf16", 8), ("f32", 16),
-                                     pytest.param("bf16", 64, marks=_D64_RAMP)])
+@pytest.mark.parametrize("dtype,d,L", [("bf16", 32, 256), ("bf16", 8, 256), ("f32", 16, 256),
+                                       ("bf16", 32, 512), ("bf16", 8, 448),
+                                       pytest.param("bf16", 64, 256, marks=_D64_RAMP)])
 @pytest.mark.parametrize("sign", [1, -1])
-def test_running_max_moves(dtype, d, sign):
+def test_running_max_moves(dtype, d, L, sign):
     """A bias ramp of 40 along the keys makes the logits of every query grow
     (sign 1: the running max is raised at many key tiles, each time by more
     than the 2^8 rescale threshold) or fall (sign -1: set by the first tile)."""
-    N, L, H = 2, 256, 2
+    N, H = 2, 2
     w, x = make_inputs(N, L, H, d, dtype, seed=21, mask="none")
     ramp = sign * np.linspace(0.0, 40.0, L)
     b = W.as_float64(x["bias"], dtype) + ramp[None, None, None, :]
@@ -210,7 +217,11 @@ def test_rows_are_independent():
 
 
 def test_unsupported_shapes_raise():
-    q = torch.zeros((2, 300, 2, 32), dtype=torch.bfloat16, device="cuda")
+    q = torch.zeros((2, 520, 2, 32), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(ea.EvoAttnError) as e:
+        ea.evo_attn_fwd(q, q, q)
+    assert e.value.status == 2
+    q = torch.zeros((2, 300, 2, 32), dtype=torch.float32, device="cuda")
     with pytest.raises(ea.EvoAttnError) as e:
         ea.evo_attn_fwd(q, q, q)
     assert e.value.status == 2

@@ -141,18 +141,25 @@ __device__ __forceinline__ void bias_block_transpose(uint16_t *tile, const u32x4
     }
 }
 
-template <typename T, int D, int NKT, bool BV>
-__global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
+// KG: key groups per unit.  A unit's NKT key tiles run as KG workgroups of
+// NKT / KG waves (each stages all of the unit's queries; the first writes
+// dA, dG and Dsum), so that a call with few (row, head) units still fills
+// the chip.  Staging then runs in KG passes of the full workgroup's batch.
+template <typename T, int D, int NKT, bool BV, int KG>
+__global__ void __launch_bounds__(NKT / KG * 64) kv_kernel(KvArgs a) {
     using E = typename Tr<T>::elem;
     using K32 = typename Tr<T>::K32;
     constexpr int ES = sizeof(E);
     constexpr int VEC = Tr<T>::VEC;
     constexpr int CPT = D / VEC;     // 16-byte chunks per token
     constexpr int LP = NKT * 32;
-    constexpr int NT = NKT * 64;
+    constexpr int NW = NKT / KG;     // waves (key tiles) per workgroup
+    constexpr int NT = NW * 64;
     constexpr int RSTR = D + VEC;    // row-major LDS stride
     constexpr int TSTR = LP + VEC;   // transposed LDS stride
-    constexpr int NST = (LP * CPT + NT - 1) / NT;  // staged 16-byte chunks per thread
+    constexpr int NST = (LP * CPT + NKT * 64 - 1) / (NKT * 64);  // staged 16-byte chunks per thread and pass
+    constexpr int NPASS = (LP * CPT + NT * NST - 1) / (NT * NST);  // staging passes
+    constexpr int NLB = (LP + NT - 1) / NT;  // lse values per thread
     // output channels per workgroup: head_dim 64 runs as two units per (row,
     // head), both forming S and dP from all 64 channels, each producing 32
     // channels of dK and dV; the first also writes dA, dG and Dsum
@@ -170,16 +177,18 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
     __shared__ __attribute__((aligned(16))) E dat_lds[kTr ? 8 : DO * TSTR];
     __shared__ __attribute__((aligned(16))) float lse2_lds[LP];
     __shared__ __attribute__((aligned(16))) float dsum_lds[LP];
-    __shared__ __attribute__((aligned(16))) uint16_t bt_lds[kBD ? NKT * 32 * 32 : 8];
+    __shared__ __attribute__((aligned(16))) uint16_t bt_lds[kBD ? NW * 32 * 32 : 8];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int h2 = lane >> 5, n = lane & 31;
     const int L = (int)a.L;
-    const int64_t unit = xcd_unit(blockIdx.x, gridDim.x);  // (row, head[, half]), head fastest
-    if (unit >= a.n_units) return;
+    const int64_t u = xcd_unit(blockIdx.x, gridDim.x);  // (row, head[, half][, key group]), key group fastest
+    if (u >= a.n_units) return;
+    const int kg = KG == 1 ? 0 : (int)(u % KG);
+    const int64_t unit = u / KG;
     const int ch = NHALF == 1 ? 0 : (int)(unit % NHALF);
     const int c_off = ch * DO;  // first output channel of the unit
-    const bool writer = ch == 0;  // writes the per-token outputs shared by the halves
+    const bool writer = ch == 0 && kg == 0;  // writes the per-token outputs shared by the halves and groups
     const int hh = (int)(unit / NHALF % a.H);
     const int64_t r = unit / NHALF / a.H;
     const int64_t b = r / a.rpb;
@@ -194,7 +203,7 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
     // ---- every load of the unit goes out first, in the order of use:
     // this wave's key tile (K, V as B operands, lane = key), its mask, the
     // lse of the staged queries, the staged tokens, the first bias tile
-    const int kt = wave;
+    const int kt = kg * NW + wave;
     const int key = kt * 32 + n;
     const bool kin = key < L;
     const uint32_t key_off = kin ? (uint32_t)key * stok_b : kOOB;
@@ -202,14 +211,19 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
     kb.load(tok_buf(a.k), key_off, h2);
     vb.load(tok_buf(a.v), key_off, h2);
     const uint32_t mbyte = bload1(has_mask ? make_buf(a.mask + r * a.L, (uint32_t)L) : none, (uint32_t)key);
-    const float lraw = __builtin_bit_cast(float, bload4(make_buf(a.lse + rh * L, (uint32_t)L * 4u),
-                                                        tid < L ? (uint32_t)tid * 4u : kOOB));
+    float lraw[NLB];
+#pragma unroll
+    for (int j = 0; j < NLB; ++j) {
+        const int t = tid + j * NT;
+        lraw[j] = __builtin_bit_cast(float, bload4(make_buf(a.lse + rh * L, (uint32_t)L * 4u),
+                                                   t < L ? (uint32_t)t * 4u : kOOB));
+    }
     u32x4 qv[NST], ov[NST], dov[NST], gv[NST];
-    {
-        const rsrc_t rq = tok_buf(a.q), ro = tok_buf(a.out), rdo = tok_buf(a.dout), rg = has_gate ? tok_buf(a.g) : none;
+    const rsrc_t rq = tok_buf(a.q), ro = tok_buf(a.out), rdo = tok_buf(a.dout), rg = has_gate ? tok_buf(a.g) : none;
+    auto load_batch = [&](int pass) {
 #pragma unroll
         for (int j = 0; j < NST; ++j) {
-            const int idx = tid + j * NT;
+            const int idx = tid + (pass * NST + j) * NT;
             const int t = idx / CPT, c = (idx % CPT) * VEC;
             const uint32_t off = (idx < LP * CPT && t < L) ? (uint32_t)t * stok_b + (uint32_t)(c * ES) : kOOB;
             qv[j] = bload16(rq, off);
@@ -217,7 +231,8 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
             dov[j] = bload16(rdo, off);
             gv[j] = bload16(rg, off);
         }
-    }
+    };
+    load_batch(0);
     // bias of this lane's key: reg i <-> query qt*32 + krow(i, h2)
     const rsrc_t rbt = has_bias ? make_buf((const E *)(kBD ? a.bias : a.biasT) + (b * a.H + hh) * (int64_t)L * L,
                                            (uint32_t)(L * L * ES))
@@ -234,8 +249,11 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
         const rsrc_t rda = make_buf((E *)a.da + rh * (int64_t)L * D, (uint32_t)(L * D * ES));
         const rsrc_t rds = make_buf(a.dsum + rh * L, (uint32_t)L * 4u);
 #pragma unroll
+        for (int pass = 0; pass < NPASS; ++pass) {
+        if (pass > 0) load_batch(pass);
+#pragma unroll
         for (int j = 0; j < NST; ++j) {
-            const int idx = tid + j * NT;
+            const int idx = tid + (pass * NST + j) * NT;
             const int t = idx / CPT, c = (idx % CPT) * VEC;
             const bool in = idx < LP * CPT;
             const bool valid = in && t < L;
@@ -279,14 +297,18 @@ __global__ void __launch_bounds__(NKT * 64) kv_kernel(KvArgs a) {
                 }
             }
         }
-        if (tid < LP)  // padded or fully masked queries: P = 0
-            lse2_lds[tid] = (tid < L && lraw != -INFINITY) ? lraw * kLog2e : INFINITY;
+        }
+#pragma unroll
+        for (int j = 0; j < NLB; ++j) {  // padded or fully masked queries: P = 0
+            const int t = tid + j * NT;
+            if (t < LP) lse2_lds[t] = (t < L && lraw[j] != -INFINITY) ? lraw[j] * kLog2e : INFINITY;
+        }
     }
     const bool kvalid = kin && (!has_mask || mbyte != 0);
     const bool kfull = __ballot(kvalid) == ~0ull;
     const float c2 = a.scale * kLog2e;
     const int arow = sig(n);  // permuted A-operand row of this lane
-    uint16_t *const bt_tile = &bt_lds[kBD ? wave * 1024 : 0];
+    uint16_t *const bt_tile = &bt_lds[kBD ? wave * 1024 : 0];  // (per wave of this workgroup)
     if constexpr (kBD) bias_block_transpose(bt_tile, braw, lane, bcur);
     __syncthreads();
 
@@ -716,12 +738,28 @@ inline bool bias_direct(const Problem &p) { return p.dtype == 1 && p.L % 8 == 0;
 // output channels over two workgroups
 inline int64_t head_halves(const Problem &p) { return p.D > 32 ? p.D / 32 : 1; }
 
+template <typename T, int D, int NKT, bool BV, int KG>
+hipError_t launch_kv(const KvArgs &ka0, hipStream_t s) {
+    KvArgs ka = ka0;
+    ka.n_units = ka0.n_units * KG;
+    hipLaunchKernelGGL((kv_kernel<T, D, NKT, BV, KG>), dim3(round8(ka.n_units)), dim3(NKT / KG * 64), 0, s, ka);
+    return hipGetLastError();
+}
+
 template <typename T, int D, int NKT, bool BV>
 hipError_t launch_passes(const Problem &p, const KvArgs &ka, const QbArgs &qa, hipStream_t s, Tracer &tr) {
     // grids are rounded up to a multiple of 8 for the XCD-aware unit order;
-    // surplus workgroups exit at once
-    hipLaunchKernelGGL((kv_kernel<T, D, NKT, BV>), dim3(round8(ka.n_units)), dim3(NKT * 64), 0, s, ka);
-    hipError_t e = hipGetLastError();
+    // surplus workgroups exit at once.  With fewer (row, head) units than
+    // two per CU, the dK/dV pass splits each unit's key tiles over two or
+    // four workgroups.
+    hipError_t e;
+    if constexpr (NKT >= 4) {
+        if (ka.n_units * 2 <= 256) e = launch_kv<T, D, NKT, BV, 4>(ka, s);
+        else if (ka.n_units < 512) e = launch_kv<T, D, NKT, BV, 2>(ka, s);
+        else e = launch_kv<T, D, NKT, BV, 1>(ka, s);
+    } else {
+        e = launch_kv<T, D, NKT, BV, 1>(ka, s);
+    }
     if (e != hipSuccess) return e;
     tr.mark(s);
     hipLaunchKernelGGL((qbias_kernel<T, D, NKT, BV>), dim3(round8(qa.n_units)), dim3(NKT * 64), 0, s, qa);

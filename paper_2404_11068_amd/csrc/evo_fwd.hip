@@ -94,8 +94,11 @@ __device__ __forceinline__ uint64_t key_lanes(uint32_t kb, int i) {
     return (lo ? 0x00000000ffffffffull : 0ull) | (hi ? 0xffffffff00000000ull : 0ull);
 }
 
-template <typename T, int D, int NKT, int KC, bool BV>
-__global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
+// QG: query groups per unit.  A unit's NKT query tiles run as QG workgroups
+// of NKT / QG waves each (all of them stage the unit's K and V), so that a
+// call with few (row, head) units still fills the chip.
+template <typename T, int D, int NKT, int KC, bool BV, int QG>
+__global__ void __launch_bounds__(NKT / QG * 64) fwd_kernel(FwdArgs a) {
     using E = typename Tr<T>::elem;
     using K32 = typename Tr<T>::K32;
     constexpr int ES = sizeof(E);
@@ -109,7 +112,9 @@ __global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
     constexpr int VEC = Tr<T>::VEC;
     constexpr int CPT = D / VEC;               // 16-byte chunks per token
     constexpr int LP = NKT * 32;
-    constexpr int NT = NKT * 64;
+    constexpr int NW = NKT / QG;               // waves (query tiles) per workgroup
+    constexpr int NT = NW * 64;
+    constexpr int NKB = (LP + NT - 1) / NT;    // keys per thread for the mask bits
     constexpr int KSTR = D + VEC;              // row stride of K / V in LDS (elements)
     constexpr int VSTR = LP + VEC;             // row stride of V^T in LDS (fp32 path)
     // bf16: V rows in LDS are 32 columns wide whatever the head dim (the
@@ -129,21 +134,24 @@ __global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int h2 = lane >> 5, n = lane & 31;
     const int L = (int)a.L;
-    const int qi = wave * 32 + n;
+    // one workgroup per (row, head[, channel half], query group) unit;
+    // consecutive units (the query groups and heads of a row) land on the
+    // same XCD
+    const int64_t u = xcd_unit(blockIdx.x, gridDim.x);
+    if (u >= a.n_units) return;
+    const int qg = QG == 1 ? 0 : (int)(u % QG);
+    const int64_t uh = u / QG;
+    const int qi = (qg * NW + wave) * 32 + n;
     const bool qvalid = qi < L;
     const bool has_bias = a.bias != nullptr, has_mask = a.mask != nullptr, has_gate = a.g != nullptr;
     const uint32_t stok_b = (uint32_t)(a.stok * ES);
     const uint32_t row_bytes = (uint32_t)(a.L * a.stok * ES);  // host: below 2^31
     const uint32_t q_off = qvalid ? (uint32_t)qi * stok_b : kOOB;
 
-    // one workgroup per (row, head[, channel half]) unit; consecutive units
-    // (the heads of a row) land on the same XCD
-    const int64_t u = xcd_unit(blockIdx.x, gridDim.x);
-    if (u >= a.n_units) return;
-    const int ch = NHALF == 1 ? 0 : (int)(u % NHALF);
+    const int ch = NHALF == 1 ? 0 : (int)(uh % NHALF);
     const int c_off = ch * DO;  // first output channel of the unit
-    const int64_t r = u / NHALF / a.H;
-    const int hh = (int)(u / NHALF % a.H);
+    const int64_t r = uh / NHALF / a.H;
+    const int hh = (int)(uh / NHALF % a.H);
     auto tok_buf = [&](const void *X) {
         return make_buf((const E *)X + r * a.srow + (int64_t)hh * D, row_bytes);
     };
@@ -163,8 +171,10 @@ __global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
             kr[j] = bload16(rk, off);
             vr[j] = bload16(rv, off);
         }
-        const uint32_t mb = bload1(has_mask ? make_buf(a.mask + r * a.L, (uint32_t)L) : make_buf(nullptr, 0u),
-                                   (uint32_t)tid);
+        const rsrc_t rmask = has_mask ? make_buf(a.mask + r * a.L, (uint32_t)L) : make_buf(nullptr, 0u);
+        uint32_t mb[NKB];
+#pragma unroll
+        for (int j = 0; j < NKB; ++j) mb[j] = bload1(rmask, (uint32_t)(tid + j * NT));
 #pragma unroll
         for (int j = 0; j < NPF; ++j) {
             const int idx = tid + j * NT;
@@ -190,11 +200,17 @@ __global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
                 *reinterpret_cast<u32x4 *>(&v_lds[t * VSTRB + DO + 8 * pc]) = w;
             }
         }
-        const bool keep = (!has_mask || mb != 0) && tid < L;
-        const unsigned long long bal = __ballot(keep);  // NT >= LP: one key per thread
-        if (lane == 0) {
-            if (2 * wave < NKT) kbits[2 * wave] = (uint32_t)bal;
-            if (2 * wave + 1 < NKT) kbits[2 * wave + 1] = (uint32_t)(bal >> 32);
+        // key-mask bits of every key tile: 64 keys per wave and step
+#pragma unroll
+        for (int j = 0; j < NKB; ++j) {
+            const int key = tid + j * NT;
+            const bool keep = (!has_mask || mb[j] != 0) && key < L;
+            const unsigned long long bal = __ballot(keep);
+            const int kt0 = (j * NT + wave * 64) / 32;
+            if (lane == 0) {
+                if (kt0 < NKT) kbits[kt0] = (uint32_t)bal;
+                if (kt0 + 1 < NKT) kbits[kt0 + 1] = (uint32_t)(bal >> 32);
+            }
         }
     }
     ChFrag<T, D> qf;
@@ -397,21 +413,35 @@ __global__ void __launch_bounds__(NKT * 64) fwd_kernel(FwdArgs a) {
 // registers (two tiles need about 130, which halves the occupancy)
 template <int NKT> constexpr int kFwdKC = 1;
 
-template <typename T, int D, int NKT, bool BV>
-hipError_t launch_t(const Problem &p, const FwdPtrs &x, hipStream_t s) {
+template <typename T, int D, int NKT, bool BV, int QG>
+hipError_t launch_q(const Problem &p, const FwdPtrs &x, hipStream_t s) {
     // unaligned bias rows are read per element, one tile per chunk
     constexpr int KC = BV ? kFwdKC<NKT> : 1;
     FwdArgs a;
     a.q = x.q; a.k = x.k; a.v = x.v; a.g = x.g; a.bias = x.bias; a.mask = x.mask;
     a.out = x.out; a.lse = x.lse;
     a.L = p.L; a.rpb = p.rpb; a.srow = p.srow; a.stok = p.stok; a.H = p.H;
-    a.n_units = p.N * p.H * (D > 32 ? D / 32 : 1);
+    a.n_units = p.N * p.H * (D > 32 ? D / 32 : 1) * QG;
     a.scale = 1.0f / sqrtf((float)D);
     // one workgroup per unit; the grid is rounded up to a multiple of 8 so
     // that the XCD-aware unit order applies (surplus workgroups exit)
     const int64_t nwg = (a.n_units + 7) / 8 * 8;
-    hipLaunchKernelGGL((fwd_kernel<T, D, NKT, KC, BV>), dim3((unsigned)nwg), dim3(NKT * 64), 0, s, a);
+    hipLaunchKernelGGL((fwd_kernel<T, D, NKT, KC, BV, QG>), dim3((unsigned)nwg), dim3(NKT / QG * 64), 0, s, a);
     return hipGetLastError();
+}
+
+// Query groups per (row, head): with fewer units than two per CU (512), a
+// unit's query tiles are split over two or four workgroups (each stages the
+// unit's K and V, mostly from the L2 its XCD shares with the unit's other
+// groups).
+template <typename T, int D, int NKT, bool BV>
+hipError_t launch_t(const Problem &p, const FwdPtrs &x, hipStream_t s) {
+    const int64_t units = p.N * p.H * (D > 32 ? D / 32 : 1);
+    if constexpr (NKT >= 4) {
+        if (units * 2 <= 256) return launch_q<T, D, NKT, BV, 4>(p, x, s);
+        if (units < 512) return launch_q<T, D, NKT, BV, 2>(p, x, s);
+    }
+    return launch_q<T, D, NKT, BV, 1>(p, x, s);
 }
 
 template <typename T, int D, int NKT>

@@ -94,6 +94,17 @@ WORKLOADS = [
              mask_p=0.05, seed=1004,
              description="extra-MSA row attention with pair bias: 1024 rows x L=256, H=8, d=8, "
                          "bias [8,256,256], 5% random key drop"),
+    # one GPU's share when the rows of a call are split over 8 GPUs (each GPU
+    # runs its rows with the whole bias plane): the kernels at their per-GPU
+    # size
+    Workload("msa_row_bias_bf16_share8", 16, 256, 8, 32, "bf16", True, 16, mask="length",
+             len_lo=224, len_hi=256, seed=1005,
+             description="one of 8 row shares of MSA row attention with pair bias: 16 rows x "
+                         "L=256, H=8, d=32, bias [8,256,256], keys beyond U{224..256} padded"),
+    Workload("extra_msa_bf16_share8", 128, 256, 8, 8, "bf16", True, 128, mask="bernoulli",
+             mask_p=0.05, seed=1006,
+             description="one of 8 row shares of extra-MSA row attention with pair bias: 128 rows "
+                         "x L=256, H=8, d=8, bias [8,256,256], 5% random key drop"),
 ]
 
 

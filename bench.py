@@ -126,6 +126,8 @@ def main():
     ap.add_argument("--workload", default="tri_start_bf16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-baseline duration")
+    ap.add_argument("--rate-calibration", action="store_true",
+                    help="only measure the vector ALU's exp2 and fma lane-op rates (evo_probe_rate)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (reference for HBM byte counters)")
     ap.add_argument("--source-hash", nargs="?", const="attn", default=None, choices=sorted(KERNEL_SOURCES),
@@ -146,6 +148,9 @@ def main():
 
     if args.copy_calibration:
         copy_calibration(torch, args.copy_calibration, max(args.steps, 1))
+        return
+    if args.rate_calibration:
+        rate_calibration(torch, max(args.steps, 1))
         return
 
     if args.workload.startswith("ln_"):
@@ -956,7 +961,7 @@ def measured_traffic(kernel: str, workload: str):
 
 # device sources of each kernel family (a change to any of them invalidates
 # the family's recorded counters)
-KERNEL_SOURCES = {"attn": ("evo_frag.h", "evo_fwd.hip", "evo_bwd.hip"),
+KERNEL_SOURCES = {"attn": ("evo_frag.h", "evo_fwd.hip", "evo_bwd.hip", "evo_bwd_fused.hip"),
                   "ln": ("evo_frag.h", "evo_ln.hip"),
                   "proj": ("evo_frag.h", "evo_proj.hip"),
                   "proj_bwd": ("evo_frag.h", "evo_proj_bwd.hip"),
@@ -988,6 +993,38 @@ def kernel_source_hash(family: str = "attn") -> str:
         with open(os.path.join(csrc, name), "rb") as f:
             h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()
+
+
+def rate_calibration(torch, steps: int):
+    """Lane operations per second of v_exp_f32 and v_fma_f32 over the whole GPU
+    (evo_probe_rate: 8 independent chains per lane, 2048 workgroups of 256
+    threads), the unit rates behind the VALU bounds of the attention kernels."""
+    from paper_2404_11068_amd import evo_attn as ea
+    lib = ea.load_library()
+    lib.evo_probe_rate.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    lib.evo_probe_rate.restype = ctypes.c_int
+    blocks, iters = 2048, 4096
+    sink = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    out = {}
+    for name, op in (("v_exp_f32", 0), ("v_fma_f32", 1)):
+        for _ in range(2):  # warm-up
+            assert lib.evo_probe_rate(op, blocks, iters, ctypes.c_void_p(sink.data_ptr()),
+                                      ctypes.c_void_p(stream.cuda_stream)) == 0
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(steps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            lib.evo_probe_rate(op, blocks, iters, ctypes.c_void_p(sink.data_ptr()), ctypes.c_void_p(stream.cuda_stream))
+            b.record(stream)
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        ms = float(np.median(ts))
+        out[name] = {"tera_lane_ops_per_s": round(blocks * 256 * 8 * iters / (ms * 1e-3) / 1e12, 2), "ms": round(ms, 4)}
+    assert bool(torch.isfinite(sink).all())
+    print(json.dumps({"rate_calibration": out, "lane_ops_per_launch": blocks * 256 * 8 * iters,
+                      "note": "8 independent chains per lane; median of %d launches" % steps}))
 
 
 def copy_calibration(torch, mib: int, steps: int):

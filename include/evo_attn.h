@@ -25,10 +25,18 @@
  * Conventions shared by every entry point
  * ---------------------------------------
  * - All tensor pointers are DEVICE pointers owned by the caller.  The library
- *   never allocates, frees or synchronises device memory, and keeps no
- *   mutable global state; every call only enqueues kernels on `stream`
- *   (a hipStream_t; NULL = the null stream), so calls may be captured into a
- *   HIP graph.  Calls return as soon as the work is enqueued.
+ *   never allocates, frees or synchronises device memory; every call only
+ *   enqueues kernels on `stream` (a hipStream_t; NULL = the null stream), so
+ *   calls may be captured into a HIP graph.  Calls return as soon as the work
+ *   is enqueued.
+ * - Process-wide state, all of it set once: the environment variable
+ *   EVO_ATTN_QBIAS_WAVES (a positive integer; default 4096) is read on the
+ *   first backward plan of the process and fixes, for the rest of the
+ *   process, how many waves the two-pass backward's dQ/dBias pass aims for
+ *   (and so its row chunks and workspace size: set it before the first
+ *   call, since evo_attn_bwd_workspace_size and evo_attn_bwd must see the
+ *   same value); and the fixed scratch of evo_attn_bwd_noalloc (below), with
+ *   its per-device address, looked up on the first such call on a device.
  * - Token tensors Q, K, V, G, O, dO, dQ, dK, dV, dG share one layout: element
  *   (r, t, h, c) lives at  base + r*stride_row + t*stride_tok + h*head_dim + c
  *   (strides in ELEMENTS; the [H, d] block of a token is contiguous).  The

@@ -24,6 +24,14 @@
  * - Every tensor pointer is a DEVICE pointer owned by the caller.  The
  *   library never allocates, frees or synchronises; each call only enqueues
  *   kernels on `stream` (a hipStream_t, NULL = the null stream) and returns.
+ * - Process-wide state, read once: the environment variables EVO_LN_FWD_WGS
+ *   and EVO_LN_BWD_WGS (positive integers) cap the forward's and the
+ *   backward's workgroup counts (default: one pass per wave for the forward,
+ *   512 for the backward).  Each is read on the first call that needs it,
+ *   once per (dtype, channel count) kernel variant, and holds for the rest of
+ *   the process; the backward's count is also its number of partial
+ *   dweight/dbias rows, so set EVO_LN_BWD_WGS before the first
+ *   evo_layernorm_bwd_workspace_size call.
  * - x, y, dy, dx are contiguous [R, C] in the working dtype (fp32 or bf16)
  *   and 16-byte aligned; weight, bias, dweight, dbias are contiguous fp32
  *   [C], 16-byte aligned; mean and rstd are contiguous fp32 [R], 4-byte

@@ -18,7 +18,7 @@ OBJDIR = os.path.join(PKG, "_build")
 
 SOURCES = ["evo_fwd.hip", "evo_bwd.hip", "evo_bwd_fused.hip", "evo_ln.hip", "evo_proj.hip", "evo_pair_bias.hip", "evo_optim.hip",
            "evo_proj_bwd.hip", "evo_pair_bias_bwd.hip",
-           "evo_api.cpp", "evo_ln_api.cpp", "evo_proj_api.cpp", "evo_optim_api.cpp", "evo_graph.cpp"]
+           "evo_probe.hip", "evo_api.cpp", "evo_ln_api.cpp", "evo_proj_api.cpp", "evo_optim_api.cpp", "evo_graph.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -203,3 +203,19 @@ def test_noalloc_backward_validates_before_any_hip_call():
     e = _dims(n_rows=0, rows_per_bias=1)
     assert _bwd_noalloc(e, q=None, k=None, v=None, out=None, lse=None, dout=None, dq=None, dk=None,
                         dv=None) == 0
+
+
+def test_probe_exported_and_validates():
+    """include/evo_probe.h: every declared symbol exported; invalid calls are
+    refused before any HIP call."""
+    lib = _lib()
+    probe = os.path.join(ROOT, "include", "evo_probe.h")
+    decls = re.findall(r"^\s*int\s+(evo_\w+)\s*\(", open(probe).read(), flags=re.M)
+    assert decls == ["evo_probe_rate"]
+    lib.evo_probe_rate.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    lib.evo_probe_rate.restype = ctypes.c_int
+    P = ctypes.c_void_p
+    assert lib.evo_probe_rate(7, 1, 1, P(FAKE), None) == 1
+    assert lib.evo_probe_rate(0, 0, 1, P(FAKE), None) == 1
+    assert lib.evo_probe_rate(0, 1, 0, P(FAKE), None) == 1
+    assert lib.evo_probe_rate(1, 1, 1, None, None) == 1

@@ -714,6 +714,32 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(4
     }
 }
 
+// The same sums four consecutive elements per thread (planes of a multiple
+// of 4 elements): 16-byte loads, four chunks' loads in flight, and still
+// chunk order for every element (the same bits as the scalar kernel).
+__global__ void __launch_bounds__(256) dbias_reduce4_kernel(const float *__restrict__ part,
+                                                         float *__restrict__ dbias, int64_t planes,
+                                                         int64_t chunks, int64_t plane_elems) {
+    const int64_t quads = plane_elems / 4;
+    const int64_t total = planes * quads;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t p = e / quads, x = (e % quads) * 4;
+        const float *src = part + p * chunks * plane_elems + x;
+        f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+        int64_t c = 0;
+        for (; c + 4 <= chunks; c += 4) {
+            f32x4 v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const f32x4 *>(src + (c + u) * plane_elems);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) acc += v[u];
+        }
+        for (; c < chunks; ++c) acc += *reinterpret_cast<const f32x4 *>(src + c * plane_elems);
+        *reinterpret_cast<f32x4 *>(dbias + p * plane_elems + x) = acc;
+    }
+}
+
 // dbias[p][x] = sum over chunks c of part[p][c][x], in chunk order
 __global__ void __launch_bounds__(256) dbias_reduce_kernel(const float *__restrict__ part, float *__restrict__ dbias,
                                                         int64_t planes /* B*H */, int64_t chunks, int64_t plane_elems) {
@@ -842,8 +868,15 @@ hipError_t launch_bwd_t(const Problem &p, const BwdPtrs &x, void *ws, const BwdP
     const int64_t pe = p.L * p.L;
     int64_t blocks = (planes * pe + 255) / 256;
     if (blocks > 8192) blocks = 8192;
-    hipLaunchKernelGGL(dbias_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, s,
-                       (const float *)(w + plan.off_part), x.dbias, planes, plan.chunks, pe);
+    if (pe % 4 == 0) {  // (dbias from the ABI and the partial planes are 16-byte aligned)
+        int64_t b4 = (planes * pe / 4 + 255) / 256;
+        if (b4 > 8192) b4 = 8192;
+        hipLaunchKernelGGL(dbias_reduce4_kernel, dim3((unsigned)b4), dim3(256), 0, s,
+                           (const float *)(w + plan.off_part), x.dbias, planes, plan.chunks, pe);
+    } else {
+        hipLaunchKernelGGL(dbias_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, s,
+                           (const float *)(w + plan.off_part), x.dbias, planes, plan.chunks, pe);
+    }
     e = hipGetLastError();
     if (e == hipSuccess) tr.mark(s);
     return e;

@@ -87,37 +87,6 @@ __device__ __forceinline__ Tr<bf16_t>::K32 ds_transpose(uint16_t *tile, const Tr
 template <int NKT, int NQR>
 constexpr int kLdsBiasTiles = NKT > NQR ? NKT - NQR : 0;
 
-// The pair bias of (query tile qt, key tile kt) as the A operand of a k32
-// product: lane m takes the bias row of query qt*32 + sig(m) (the permuted
-// rows of the Q operand of S = Q K^T), k-slots = keys kt*32 + {8h+s, 16+8h+s},
-// as it lies in memory.  Times sqrt(d) on an identity B operand it adds
-// sqrt(d) * bias to the logit tile whose lanes own keys.  BV: rows of whole
-// 16-byte groups (two loads per lane); otherwise one element per load.  Rows
-// and keys past L read zeros.
-template <bool BV>
-__device__ __forceinline__ Tr<bf16_t>::K32 bias_rows_k32(rsrc_t rb, int L, int qt, int kt, int lane) {
-    const int m = lane & 31, h = lane >> 5;
-    const int qi = qt * 32 + sig(m);
-    const int k0 = kt * 32 + 8 * h;
-    Tr<bf16_t>::K32 f;
-    if constexpr (BV) {
-        f.v[0] = __builtin_bit_cast(bf16x8, bload16(rb, qi < L ? (uint32_t)(qi * L + k0) * 2u : kOOB));
-        f.v[1] = __builtin_bit_cast(bf16x8, bload16(rb, qi < L ? (uint32_t)(qi * L + k0 + 16) * 2u : kOOB));
-    } else {
-        short8tr w[2];
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int kj = k0 + 16 * t + e;
-                w[t][e] = (short)bload2(rb, (qi < L && kj < L) ? (uint32_t)(qi * L + kj) * 2u : kOOB);
-            }
-        f.v[0] = __builtin_bit_cast(bf16x8, w[0]);
-        f.v[1] = __builtin_bit_cast(bf16x8, w[1]);
-    }
-    return f;
-}
-
 template <int D, int NKT, bool HB, bool BV, int NQR>
 __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
     using E = uint16_t;

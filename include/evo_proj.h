@@ -3,9 +3,10 @@
  *
  * The step in front of every Evoformer attention: normalise the input
  * representation and project it to queries, keys, values and gate logits.
- * ScaleFold (arXiv 2404.11068), Section 3.3: the four linear layers have no
- * dependency on each other, so they run as one batched product ("GEMM
- * Batching"), fused with the LayerNorm that precedes them.  Computed here:
+ * ScaleFold (arXiv 2404.11068), Section 3.3, GEMM Batching: the query, key,
+ * value and gate projections read the same input and none needs another's
+ * result, so they run as one batched product, fused here with the LayerNorm
+ * in front of them.  Computed here:
  *
  *   y        = LayerNorm(x) over the last axis (as in evo_layernorm.h), bf16
  *   out_p    = y @ weight[p*HD : (p+1)*HD, :]^T + bias[p*HD : (p+1)*HD]

@@ -178,8 +178,9 @@ def layernorm_backward(x, dy, weight=None, eps: float = 1e-5):
 def ln_proj_forward(x, ln_weight, ln_bias, weight, bias=None, n_proj: int = 1, eps: float = 1e-5):
     """LayerNorm over the last axis followed by n_proj independent linear
     projections that share the normalised input (ScaleFold Section 3.3,
-    "GEMM Batching": the four linear layers in front of the attention have
-    no dependency on each other and run as one batched product).
+    GEMM Batching: the query, key, value and gate projections in front of
+    the attention are mutually independent, so they form one batched
+    product).
 
     x [..., C]; weight [n_proj * HD, C] (torch Linear layout: row f of
     projection p is weight[p * HD + f]); bias [n_proj * HD] or None.

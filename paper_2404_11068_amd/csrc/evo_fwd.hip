@@ -37,6 +37,7 @@
 // before the current tile's math), which keeps the compiler's in-order load
 // counters exact.
 #include <math.h>
+#include <stdlib.h>
 
 #include "evo_frag.h"
 #include "evo_kernels.h"
@@ -409,6 +410,269 @@ __global__ void __launch_bounds__(NKT / QG * 64) fwd_kernel(FwdArgs a) {
             (h2 == 0 && qvalid && ch == 0) ? (uint32_t)qi * 4u : kOOB);
 }
 
+// ---------------------------------------------------------------------------
+// Row-walking forward for a pair bias shared by all rows (bf16, head_dim <=
+// 32, at most 256 keys).  A fixed grid of workgroups, its size a multiple of
+// the head count, walks the units u, u + G, u + 2G, ... (G = grid size): all
+// units of a workgroup are rows of one head under the one bias plane.  Each
+// wave loads its query tile's bias rows once, into registers (the K32
+// operands of every key tile, about 64 registers at 256 keys), and reuses
+// them for every row it visits, so the pair bias leaves L2 once per
+// workgroup instead of once per (row, head).  The next unit's K, V, key mask
+// and query tile are requested during the current unit's first key tile and
+// held in registers until that unit is staged; the gate during the last key
+// tile; each key tile reads the next tile's K and V^T operands and mask word
+// from LDS before its own math.  Per-workgroup constants (the bias diagonal
+// operands, the constant columns of the V tile) are set up once.  Per key
+// tile, against the one-unit kernel above: the masked-key operand is one LDS
+// word (written at staging), the tile max is a chain of three-input maxima,
+// the two lane halves exchange their maxima only when some lane's own
+// maximum calls for a raise of the reference max (no lane's own maximum
+// above the threshold means no combined one is), and the exponent offset
+// changes only with that max.  Every value is computed as in the one-unit
+// kernel: the outputs are the same bits.
+template <int D, int NKT>
+__global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(2))) fwd_rows_kernel(FwdArgs a) {
+    using T = bf16_t;
+    using E = uint16_t;
+    using K32 = Tr<bf16_t>::K32;
+    static_assert(D == 8 || D == 16 || D == 32, "bf16 head_dim up to 32");
+    static_assert(NKT <= 8, "bias rows of up to 256 keys in registers");
+    constexpr int VEC = 8;
+    constexpr int CPT = D / VEC;               // 16-byte chunks per token
+    constexpr int LP = NKT * 32;
+    constexpr int NT = NKT * 64;               // two threads per key: one key-mask byte each suffices
+    constexpr int KSTR = D + VEC;              // row stride of K in LDS (elements)
+    constexpr int VSTRB = 32 + VEC;            // V rows: 32 columns (data, then constants), padded
+    constexpr int PCH = (32 - D) / 8;          // constant 16-byte chunks per V row
+    constexpr bool kOnesRow = D < 32;          // row sums come out of the PV product
+    constexpr int NPF = (LP * CPT + NT - 1) / NT;
+    __shared__ __attribute__((aligned(16))) E k_lds[LP * KSTR];
+    __shared__ __attribute__((aligned(16))) E v_lds[LP * VSTRB];
+    __shared__ uint32_t mneg_lds[LP];          // masked-key operand per key: -2^64 (bf16, low half) or 0
+    __shared__ uint32_t kbits[NKT];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int h2 = lane >> 5, n = lane & 31;
+    const int L = (int)a.L;
+    const int qi = wave * 32 + n;
+    const bool qvalid = qi < L;
+    const bool has_mask = a.mask != nullptr, has_gate = a.g != nullptr;
+    const uint32_t stok_b = (uint32_t)(a.stok * 2);
+    const uint32_t row_bytes = (uint32_t)(a.L * a.stok * 2);  // host: below 2^31
+    const uint32_t q_off = qvalid ? (uint32_t)qi * stok_b : kOOB;
+    const rsrc_t none = make_buf(nullptr, 0u);
+
+    // ---- per-workgroup constants
+    const float c2 = a.scale * kLog2e;
+    float sq_hi, sq_lo;
+    sqrt_split(D, sq_hi, sq_lo);
+    const bool two_term = sq_lo != 0.0f;
+    const K32 dhi = diag_k32(sq_hi, lane);
+    K32 dlo{};
+    if (two_term) dlo = diag_k32(sq_lo, lane);
+    // B operand of the masked-key term: 1 in k-slot 0 (lane half 0), zeros
+    // elsewhere, so only the A operand's slot 0 (the key's mask word) counts
+    const short4v mask_b = {h2 == 0 ? kBf16One : (short)0, 0, 0, 0};
+    if constexpr (PCH > 0) {
+        for (int idx = tid; idx < LP * PCH; idx += NT) {
+            const int t = idx / PCH, pc = idx % PCH;
+            const u32x4 w = {(pc == 0 && kOnesRow) ? (uint32_t)(uint16_t)kBf16One : 0u, 0u, 0u, 0u};
+            *reinterpret_cast<u32x4 *>(&v_lds[t * VSTRB + D + 8 * pc]) = w;
+        }
+    }
+
+    // unit u -> (row ur, head uh), advanced incrementally: u grows by G per step
+    const int H = a.H;
+    const int64_t G = gridDim.x;
+    const int64_t GH = G / H;
+    const int Gh = (int)(G % H);  // 0: the host makes G a multiple of H
+    int64_t u = xcd_unit(blockIdx.x, G);
+    int64_t ur = u / H;
+    int uh = (int)(u % H);
+    // first element of a unit's [L, d] block in the token tensors; a unit past
+    // the last one gets an empty resource (its loads read zeros)
+    auto tok_buf = [&](const void *X, int64_t tb, bool ok) {
+        return make_buf((const E *)X + (ok ? tb : 0), ok ? row_bytes : 0u);
+    };
+
+    // ---- this wave's bias rows (query tile `wave`, every key tile), once;
+    // the host guarantees a single plane: plane 0 for every row
+    K32 breg[NKT];
+    {
+        const rsrc_t rb = u < a.n_units ? make_buf((const E *)a.bias + (int64_t)uh * L * L, (uint32_t)(L * L * 2))
+                                        : none;
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt) breg[kt] = bias_k32<true>(rb, qi, kt, L, h2);
+    }
+
+    // ---- the in-flight unit's K, V, key-mask byte and query tile
+    u32x4 kr[NPF], vr[NPF];
+    uint32_t mr;
+    ChFrag<T, D> qn;
+    auto issue_unit = [&](int64_t rr, int h, bool ok) {
+        const int64_t tb = rr * a.srow + (int64_t)h * D;
+        const rsrc_t rk = tok_buf(a.k, tb, ok), rv = tok_buf(a.v, tb, ok);
+#pragma unroll
+        for (int j = 0; j < NPF; ++j) {
+            const int idx = tid + j * NT;
+            const int t = idx / CPT, c = (idx % CPT) * VEC;
+            const uint32_t off = (idx < LP * CPT && t < L) ? (uint32_t)t * stok_b + (uint32_t)(c * 2) : kOOB;
+            kr[j] = bload16(rk, off);
+            vr[j] = bload16(rv, off);
+        }
+        const rsrc_t rm = (has_mask && ok) ? make_buf(a.mask + rr * a.L, (uint32_t)L) : none;
+        mr = bload1(rm, (uint32_t)tid);
+        qn.load(tok_buf(a.q, tb, ok), q_off, h2);
+    };
+
+    // every load is issued whether or not a mask or gate exists (an empty
+    // resource reads zeros): a load behind a branch would leave the
+    // compiler's in-order load counters unknown after the join, and it would
+    // then wait for every load in flight, prefetches included
+    issue_unit(ur, uh, u < a.n_units);
+    for (; u < a.n_units; u += G) {
+        const int64_t tb = ur * a.srow + (int64_t)uh * D;
+        int64_t rn = ur + GH;
+        int hn = uh + Gh;
+        if (hn >= H) { hn -= H; ++rn; }
+        const bool okn = u + G < a.n_units;
+        __syncthreads();  // the previous unit's reads of the LDS tiles are done
+        // ---- stage the unit: registers -> LDS, key-mask words and bits
+#pragma unroll
+        for (int j = 0; j < NPF; ++j) {
+            const int idx = tid + j * NT;
+            if (idx < LP * CPT) {
+                const int t = idx / CPT, c = (idx % CPT) * VEC;
+                *reinterpret_cast<u32x4 *>(&k_lds[t * KSTR + c]) = kr[j];
+                *reinterpret_cast<u32x4 *>(&v_lds[t * VSTRB + c]) = vr[j];
+            }
+        }
+        {
+            const bool keep = (!has_mask || mr != 0) && tid < L;
+            if (tid < LP) mneg_lds[tid] = keep ? 0u : (uint32_t)(uint16_t)kBf16MaskNeg;
+            const unsigned long long bal = __ballot(keep);
+            if (lane == 0) {
+                if (2 * wave < NKT) kbits[2 * wave] = (uint32_t)bal;
+                if (2 * wave + 1 < NKT) kbits[2 * wave + 1] = (uint32_t)(bal >> 32);
+            }
+        }
+        const ChFrag<T, D> qf = qn;
+        __syncthreads();
+
+        u32x4 graw = {0u, 0u, 0u, 0u}, graw2 = {0u, 0u, 0u, 0u};
+        float m2 = -INFINITY;  // reference max, base-2 exponent units (per query)
+        float nm2 = 0.0f;      // exponent offset: -m2 once m2 is finite
+        float lsum = 0.0f;     // row sum (head_dim 32: no ones row)
+        f32x16 o = zero16();
+        // the unit's key-tile mask words, and the first tile's LDS operands;
+        // each tile then reads the next tile's operands before its own math
+        uint32_t kbs[NKT];
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt) kbs[kt] = __builtin_amdgcn_readfirstlane(kbits[kt]);
+        ChFrag<T, D> kf_n;
+        kf_n.load(&k_lds[sig(n) * KSTR], h2);
+        uint32_t mw_n = mneg_lds[sig(n)];
+        K32 va_n = load_k32_tr(v_lds, VSTRB, 0, 32, lane);
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt) {
+            const ChFrag<T, D> kf = kf_n;
+            const uint32_t mwv = mw_n;
+            const K32 va = va_n;
+            if (kt + 1 < NKT) {
+                kf_n.load(&k_lds[((kt + 1) * 32 + sig(n)) * KSTR], h2);
+                mw_n = mneg_lds[(kt + 1) * 32 + sig(n)];
+                va_n = load_k32_tr(v_lds, VSTRB, (kt + 1) * 32, 32, lane);
+            }
+            // ---- global loads, in the order they are waited for
+            if (kt == 0) issue_unit(rn, hn, okn);
+            if (kt == NKT - 1) {
+                const rsrc_t rg = has_gate ? tok_buf(a.g, tb, true) : none;
+                graw = bload16(rg, 8 * h2 < D ? q_off + (uint32_t)(8 * h2 * 2) : kOOB);
+                if constexpr (D > 16) graw2 = bload16(rg, q_off + (uint32_t)((16 + 8 * h2) * 2));
+            }
+            const uint32_t kb = kbs[kt];
+            if (kb != 0) {
+                f32x16 s = zero16();
+                ChFrag<T, D>::mma(s, kf, qf);
+                Tr<bf16_t>::mma_k32(s, dhi, breg[kt]);
+                if (two_term) Tr<bf16_t>::mma_k32(s, dlo, breg[kt]);
+                if (kb != 0xffffffffu) {
+                    // masked keys: -2^64 on their rows (row n of the tile is key sig(n))
+                    const u32x2 mw = {mwv, 0u};
+                    s = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(__builtin_bit_cast(short4v, mw), mask_b, s, 0, 0, 0);
+                }
+                float mx = fmaxf(fmaxf(s[0], s[1]), s[2]);
+#pragma unroll
+                for (int i = 3; i < 15; i += 2) mx = fmaxf(fmaxf(mx, s[i]), s[i + 1]);
+                mx = fmaxf(mx, s[15]);
+                // raise the reference max only where the tile max exceeds it by
+                // more than 2^kTau (always at the first finite max)
+                if (__ballot(mx * c2 > m2 + kTau)) {
+                    const float mxl = fmaxf(mx, __shfl_xor(mx, 32)) * c2;
+                    const bool need = mxl > m2 + kTau;
+                    const float alpha = need ? (m2 == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2 - mxl)) : 1.0f;
+                    if (need) m2 = mxl;
+                    nm2 = (m2 == -INFINITY) ? 0.0f : -m2;
+                    lsum *= alpha;
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) o[i] *= alpha;
+                }
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[i], c2, nm2));
+                    s[i] = p;
+                    if constexpr (!kOnesRow) lsum += p;
+                }
+                const K32 pb = Tr<T>::pack(s);
+                Tr<T>::mma_k32(o, va, pb);
+            }
+        }
+        if constexpr (kOnesRow) {
+            // channel D of O^T is the row sum: register 8*(D/16) + D%8 of lane half (D/8)%2
+            constexpr int ri = 8 * (D / 16) + D % 8, rh = (D / 8) % 2;
+            const float own = o[ri], other = __shfl_xor(own, 32);
+            lsum = (h2 == rh) ? own : other;
+        } else {
+            lsum += __shfl_xor(lsum, 32);
+        }
+
+        // ---- epilogue: normalise, gate, store O and lse
+        const float inv = lsum > 0.0f ? __builtin_amdgcn_rcpf(lsum) : 0.0f;
+        const rsrc_t ro = tok_buf(a.out, tb, true);
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            const int cb = 16 * half + 8 * h2;
+            if (16 * half >= D) continue;
+            const uint32_t off = cb < D ? q_off + (uint32_t)(cb * 2) : kOOB;
+            const u32x4 w = half == 0 ? graw : graw2;
+            const uint32_t ws[4] = {w.x, w.y, w.z, w.w};  // integer components (no bit_cast of a component)
+            float val[8];
+#pragma unroll
+            for (int s2 = 0; s2 < 4; ++s2) {
+                const float g0 = __builtin_bit_cast(float, ws[s2] << 16);
+                const float g1 = __builtin_bit_cast(float, ws[s2] & 0xffff0000u);
+                const float sg0 = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-g0 * kLog2e));
+                const float sg1 = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-g1 * kLog2e));
+                val[2 * s2] = o[8 * half + 2 * s2] * inv * (has_gate ? sg0 : 1.0f);
+                val[2 * s2 + 1] = o[8 * half + 2 * s2 + 1] * inv * (has_gate ? sg1 : 1.0f);
+            }
+            u32x4 wo;
+            wo.x = (uint32_t)f2bf(val[0]) | ((uint32_t)f2bf(val[1]) << 16);
+            wo.y = (uint32_t)f2bf(val[2]) | ((uint32_t)f2bf(val[3]) << 16);
+            wo.z = (uint32_t)f2bf(val[4]) | ((uint32_t)f2bf(val[5]) << 16);
+            wo.w = (uint32_t)f2bf(val[6]) | ((uint32_t)f2bf(val[7]) << 16);
+            bstore16(wo, ro, off);
+        }
+        // lse in natural-log units: (m2 + log2 lsum) * ln 2
+        const float lse = lsum > 0.0f ? (m2 + __builtin_amdgcn_logf(lsum)) * kLn2 : -INFINITY;
+        bstore4(__builtin_bit_cast(uint32_t, lse), make_buf(a.lse + (ur * H + uh) * a.L, (uint32_t)L * 4u),
+                (h2 == 0 && qvalid) ? (uint32_t)qi * 4u : kOOB);
+        ur = rn;
+        uh = hn;
+    }
+}
+
 // key tiles per register-resident chunk: one keeps the kernel near 90
 // registers (two tiles need about 130, which halves the occupancy)
 template <int NKT> constexpr int kFwdKC = 1;
@@ -430,6 +694,31 @@ hipError_t launch_q(const Problem &p, const FwdPtrs &x, hipStream_t s) {
     return hipGetLastError();
 }
 
+// Row-walking kernel: eligible when every row uses one bias plane, rows are
+// 16-byte aligned (bf16, L % 8 == 0), at most 256 keys, and there are at
+// least two units per resident workgroup (one 8-wave workgroup per CU at
+// the kernel's two waves per SIMD: 256 CUs x 8 waves).  EVO_ATTN_FWD_ROWS=0
+// in the environment at the time of the call selects the one-unit kernel
+// instead (same results; read on every call, no state kept).
+constexpr int64_t kRowsResidentWaves = 256 * 8;
+
+inline bool fwd_rows_enabled() {
+    const char *e = getenv("EVO_ATTN_FWD_ROWS");
+    return !(e && e[0] == '0');
+}
+
+template <int D, int NKT>
+hipError_t launch_rows(const Problem &p, const FwdPtrs &x, hipStream_t s, int64_t g) {
+    FwdArgs a;
+    a.q = x.q; a.k = x.k; a.v = x.v; a.g = x.g; a.bias = x.bias; a.mask = x.mask;
+    a.out = x.out; a.lse = x.lse;
+    a.L = p.L; a.rpb = p.rpb; a.srow = p.srow; a.stok = p.stok; a.H = p.H;
+    a.n_units = p.N * p.H;
+    a.scale = 1.0f / sqrtf((float)D);
+    hipLaunchKernelGGL((fwd_rows_kernel<D, NKT>), dim3((unsigned)g), dim3(NKT * 64), 0, s, a);
+    return hipGetLastError();
+}
+
 // Query groups per (row, head): with fewer units than two per CU (512), a
 // unit's query tiles are split over two or four workgroups (each stages the
 // unit's K and V, mostly from the L2 its XCD shares with the unit's other
@@ -437,6 +726,15 @@ hipError_t launch_q(const Problem &p, const FwdPtrs &x, hipStream_t s) {
 template <typename T, int D, int NKT, bool BV>
 hipError_t launch_t(const Problem &p, const FwdPtrs &x, hipStream_t s) {
     const int64_t units = p.N * p.H * (D > 32 ? D / 32 : 1);
+    if constexpr (sizeof(typename Tr<T>::elem) == 2 && D <= 32 && BV && NKT <= 8) {
+        // grid: the resident workgroups, a multiple of 8 (XCD-aware order)
+        // and of the head count (every workgroup keeps one head)
+        const int64_t g0 = kRowsResidentWaves / NKT;
+        const int64_t g = g0 / 8 / p.H * 8 * p.H;
+        if (x.bias != nullptr && p.rpb >= p.N && g > 0 && units >= 2 * g0 && p.N < (int64_t(1) << 31) &&
+            fwd_rows_enabled())
+            return launch_rows<D, NKT>(p, x, s, g);
+    }
     if constexpr (NKT >= 4) {
         if (units * 2 <= 256) return launch_q<T, D, NKT, BV, 4>(p, x, s);
         if (units < 512) return launch_q<T, D, NKT, BV, 2>(p, x, s);

@@ -84,6 +84,40 @@ def test_small_ragged_parity(case):
     compare(got, ref, dtype, label=str(case))
 
 
+# Shapes that select the row-walking forward (all rows under one bias plane,
+# bf16, L a multiple of 8, at most 256 keys, at least two (row, head) units
+# per resident workgroup): it must produce the bits of the one-unit kernel,
+# which the environment switch EVO_ATTN_FWD_ROWS=0 selects.  The full-size
+# workloads with a shared bias (MSA row, triangle, extra-MSA) run it against
+# the oracle in test_full_workload_parity.
+ROWS = [
+    # N, L, H, d, kwargs
+    (128, 256, 4, 32, dict()),                      # 8 key tiles, 512 units
+    (64, 200, 8, 8, dict(p=0.2)),                   # ragged last key tile
+    (96, 248, 8, 16, dict(gate=False, mask="length")),
+    (256, 104, 4, 16, dict(mask="none")),           # 4 key tiles
+    (512, 40, 4, 8, dict(mask="tail_pad")),         # 2 key tiles
+    (1024, 24, 4, 32, dict()),                      # 1 key tile
+]
+
+
+@pytest.mark.parametrize("case", ROWS, ids=lambda c: "N%dL%dH%dd%d" % c[:4])
+def test_row_walking_forward_matches_one_unit_kernel(case, monkeypatch):
+    N, L, H, d, kw = case
+    w, x = make_inputs(N, L, H, d, "bf16", seed=11 + L, **kw)
+    print("\n[case] row-walking forward", case, flush=True)
+    dev = {n: to_device(x[n], "bf16") for n in ("q", "k", "v", "gate", "bias")}
+    mask = None if x["mask"] is None else torch.from_numpy(x["mask"]).cuda()
+    args = (dev["q"], dev["k"], dev["v"], dev["gate"], dev["bias"], mask)
+    monkeypatch.setenv("EVO_ATTN_FWD_ROWS", "0")
+    out0, lse0 = ea.evo_attn_fwd(*args, rows_per_bias=w.rows_per_bias)
+    monkeypatch.setenv("EVO_ATTN_FWD_ROWS", "1")
+    out1, lse1 = ea.evo_attn_fwd(*args, rows_per_bias=w.rows_per_bias)
+    torch.cuda.synchronize()
+    assert torch.equal(out0.view(torch.int16), out1.view(torch.int16))
+    assert torch.equal(lse0, lse1)
+
+
 @pytest.mark.parametrize("d", [32, 64])
 def test_ending_node_transposed_view(d):
     """Triangle attention around the ending node: rows are the columns of the

@@ -167,6 +167,11 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
         auto tok_buf = [&](const void *X) {
             return make_buf((const E *)X + r * a.srow + (int64_t)hh * D, row_bytes);
         };
+        // per-row opaque copies of the lane's bias-row offset (query sig(n) of
+        // tile 0, this wave's keys) and thread index: each query tile's bias
+        // and dQ addresses are formed from them inside the tile's step
+        const uint32_t boff = opaque_u32((uint32_t)((sig(n) * L + kt * 32 + 8 * h2) * ES));
+        const int tid_r = (int)opaque_u32((uint32_t)tid);
         // ---- every load of the row goes out first, in the order of use
         ChFrag<bf16_t, D> kb, vb;
         kb.load(tok_buf(a.k), key_off, h2);
@@ -191,7 +196,10 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
         }
         // first query tile's bias rows
         K32 bnext;
-        if constexpr (HB) bnext = bias_rows_k32<BV>(rb, L, 0, kt, lane);
+        if constexpr (HB) {
+            if constexpr (BV) bnext = bias_rows_k32_at(rb, boff);
+            else bnext = bias_rows_k32<BV>(rb, L, 0, kt, lane);
+        }
 
         // ---- staging: Q and dA into LDS; dA, Dsum and dG from dO, O and G
         {
@@ -255,7 +263,10 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
             K32 bcur;
             if constexpr (HB) {
                 bcur = bnext;
-                if (qt + 1 < NKT) bnext = bias_rows_k32<BV>(rb, L, qt + 1, kt, lane);
+                if (qt + 1 < NKT) {
+                    if constexpr (BV) bnext = bias_rows_k32_at(rb, boff + (uint32_t)((qt + 1) * 32 * L * ES));
+                    else bnext = bias_rows_k32<BV>(rb, L, qt + 1, kt, lane);
+                }
             }
             f32x16 dq = zero16();
             if (kany) {
@@ -341,7 +352,7 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
             }
             __syncthreads();
             // the sum of tile qt is taken by the threads from wave qt % NKT on
-            const int rot = (tid + NT - (qt % NKT) * 64) % NT;
+            const int rot = (tid_r + NT - (qt % NKT) * 64) % NT;
 #pragma unroll
             for (int j = 0; j < NSUM; ++j) {  // four consecutive channels per thread and step
                 const int idx = rot + j * NT;

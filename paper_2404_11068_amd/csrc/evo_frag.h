@@ -383,6 +383,27 @@ __device__ __forceinline__ Tr<bf16_t>::K32 bias_rows_k32(rsrc_t rb, int L, int q
     return f;
 }
 
+// bias_rows_k32<true> with the byte offset of the lane's first group given
+// (query row * L + first key) * 2: tiles further down add a constant to it,
+// and rows past L land past the end of the resource (zeros).
+__device__ __forceinline__ Tr<bf16_t>::K32 bias_rows_k32_at(rsrc_t rb, uint32_t off) {
+    Tr<bf16_t>::K32 f;
+    f.v[0] = __builtin_bit_cast(bf16x8, bload16(rb, off));
+    f.v[1] = __builtin_bit_cast(bf16x8, bload16(rb, off + 32u));
+    return f;
+}
+
+// An opaque copy of a per-lane value: the compiler cannot see through it, so
+// what is computed from the copy stays inside the loop that makes the copy.
+// Used where hoisting loop-invariant addresses (one per unrolled step) out of
+// a loop would hold more registers than the loop can spare: spilled
+// addresses come back through scratch loads, and waiting for those waits for
+// every memory operation in flight.
+__device__ __forceinline__ uint32_t opaque_u32(uint32_t x) {
+    asm volatile("" : "+v"(x));
+    return x;
+}
+
 // ---------------------------------------------------------------------------
 // Constant A operand "c times a permuted identity" for the k32 contraction:
 // A[m][k] = c where k-slot k holds row sig(m) of the tile, else 0.  With a B

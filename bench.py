@@ -56,6 +56,25 @@ def fused_backward(w, es: int) -> bool:
     return nkt <= 4 or (w.head_dim == 8 and w.seq_len % 8 == 0)
 
 
+def forward_kernel(w, es: int) -> str:
+    """The forward kernel the library runs for this workload: the row-walking
+    kernel (bias rows held in registers across the rows of one head) for bf16
+    at head_dim <= 32 and at most 256 keys in 16-byte rows, when all rows
+    share one bias plane and there are at least two (row, head) units per
+    resident workgroup; the one-unit kernel otherwise."""
+    if es != 2 or w.head_dim > 32 or not w.bias or w.seq_len % 8 or w.seq_len > 256:
+        return "fwd_kernel"
+    if w.rows_per_bias < w.n_rows:
+        return "fwd_kernel"
+    nkt = 1
+    while nkt * 32 < w.seq_len:
+        nkt *= 2
+    g0 = 256 * 8 // nkt
+    g = g0 // 8 // w.n_heads * 8 * w.n_heads
+    units = w.n_rows * w.n_heads
+    return "fwd_rows_kernel" if g > 0 and units >= 2 * g0 else "fwd_kernel"
+
+
 def kernel_model(w, es: int, ws_bytes: int):
     """Per-launch traffic and MFMA flops of every kernel of one step, in launch
     order, as (name, algorithmic bytes, workspace bytes, flops).
@@ -75,7 +94,7 @@ def kernel_model(w, es: int, ws_bytes: int):
     mask = N * L if w.mask != "none" else 0
     g = 1 if w.gate else 0
     S = N * H * L * L  # logits
-    fwd = ("fwd_kernel", (3 + g) * T + bias + mask + T + lse, 0, 4.0 * S * d)
+    fwd = (forward_kernel(w, es), (3 + g) * T + bias + mask + T + lse, 0, 4.0 * S * d)
     if fused_backward(w, es):
         # one pass: reads Q K V O dO [G] lse bias mask, writes dQ dK dV [dG]
         # (and dBias itself when each plane is one row chunk); workspace:
@@ -307,6 +326,8 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
+        print("[bench] GPU timing done; timing the CPU oracle (about %.0f s)" % args.cpu_seconds,
+              file=sys.stderr, flush=True)
         cpu = cpu_baseline(w, x, args.cpu_seconds)
 
     line = {
@@ -1080,12 +1101,14 @@ def cpu_baseline(w, x, target_s: float):
     # a sample of at least one whole bias plane keeps whole planes
     if w.bias and want >= w.rows_per_bias:
         want = (want // w.rows_per_bias) * w.rows_per_bias
-    # the same sample three times (more when one run is short), median taken
+    # the same sample three times (more when one run is short, at most 25),
+    # median taken; t_run estimates one run of the sample from the probe
     reps = 3
-    if want == w.n_rows and 3 * t < target_s:  # the whole workload is short: repeat it
-        reps = max(3, int(target_s / max(t, 1e-3)))
-    elif t > target_s / 3:                    # keep three runs near the target
-        want = max(1, int(want * target_s / (3 * t)))
+    t_run = t * want / rows
+    if want == w.n_rows and 3 * t_run < target_s:  # the whole workload is short: repeat it
+        reps = min(25, max(3, int(target_s / max(t_run, 1e-3))))
+    elif t_run > target_s / 3:                    # keep three runs near the target
+        want = max(1, int(want * target_s / (3 * t_run)))
         if w.bias and want >= w.rows_per_bias:
             want = (want // w.rows_per_bias) * w.rows_per_bias
     split.clear()

@@ -776,11 +776,12 @@ template <typename T, int D, int NKT, bool BV>
 hipError_t launch_passes(const Problem &p, const KvArgs &ka, const QbArgs &qa, hipStream_t s, Tracer &tr) {
     // grids are rounded up to a multiple of 8 for the XCD-aware unit order;
     // surplus workgroups exit at once.  With fewer (row, head) units than
-    // two per CU, the dK/dV pass splits each unit's key tiles over two or
-    // four workgroups.
+    // two per CU, the dK/dV pass splits each unit's key tiles over two
+    // workgroups, over four at 64 units or fewer (at 128 units two were
+    // faster than four: each group stages the whole row's Q, dO, O and G)
     hipError_t e;
     if constexpr (NKT >= 4) {
-        if (ka.n_units * 2 <= 256) e = launch_kv<T, D, NKT, BV, 4>(ka, s);
+        if (ka.n_units <= 64) e = launch_kv<T, D, NKT, BV, 4>(ka, s);
         else if (ka.n_units < 512) e = launch_kv<T, D, NKT, BV, 2>(ka, s);
         else e = launch_kv<T, D, NKT, BV, 1>(ka, s);
     } else {
@@ -921,10 +922,14 @@ BwdPlan plan_bwd(const Problem &p, bool has_bias, size_t cap) {
         const long v = env ? atol(env) : 0;
         return v > 0 ? (int64_t)v : (int64_t)4096;
     }();
+    // Row chunks of at least four rows: with fewer rows per workgroup the
+    // per-workgroup staging and the reduction of the partial planes cost more
+    // than the extra workgroups gain (16 rows over 8 heads: 4 chunks beat 8)
     int64_t chunks = 0;
     if (planes > 0 && rpb > 0 && nqt > 0) {
         const int64_t per_chunk = planes * p.H * nqt * waves * head_halves(p);  // waves per row chunk
         chunks = (target_waves + per_chunk - 1) / per_chunk;
+        if (chunks > rpb / 4) chunks = rpb / 4;
         if (chunks < 1) chunks = 1;
         if (chunks > rpb) chunks = rpb;
     }

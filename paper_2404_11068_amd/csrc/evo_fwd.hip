@@ -720,9 +720,9 @@ hipError_t launch_rows(const Problem &p, const FwdPtrs &x, hipStream_t s, int64_
 }
 
 // Query groups per (row, head): with fewer units than two per CU (512), a
-// unit's query tiles are split over two or four workgroups (each stages the
-// unit's K and V, mostly from the L2 its XCD shares with the unit's other
-// groups).
+// unit's query tiles are split over two workgroups, over four at 64 units or
+// fewer (each stages the unit's K and V, mostly from the L2 its XCD shares
+// with the unit's other groups; at 128 units two were faster than four).
 template <typename T, int D, int NKT, bool BV>
 hipError_t launch_t(const Problem &p, const FwdPtrs &x, hipStream_t s) {
     const int64_t units = p.N * p.H * (D > 32 ? D / 32 : 1);
@@ -736,7 +736,7 @@ hipError_t launch_t(const Problem &p, const FwdPtrs &x, hipStream_t s) {
             return launch_rows<D, NKT>(p, x, s, g);
     }
     if constexpr (NKT >= 4) {
-        if (units * 2 <= 256) return launch_q<T, D, NKT, BV, 4>(p, x, s);
+        if (units <= 64) return launch_q<T, D, NKT, BV, 4>(p, x, s);
         if (units < 512) return launch_q<T, D, NKT, BV, 2>(p, x, s);
     }
     return launch_q<T, D, NKT, BV, 1>(p, x, s);

@@ -98,7 +98,18 @@ ROWS = [
     (256, 104, 4, 16, dict(mask="none")),           # 4 key tiles
     (512, 40, 4, 8, dict(mask="tail_pad")),         # 2 key tiles
     (1024, 24, 4, 32, dict()),                      # 1 key tile
+    (200, 256, 3, 16, dict(mask="length")),         # 3 heads: a grid of 240 workgroups
 ]
+
+
+def test_forward_with_several_bias_planes_at_scale():
+    """Enough units for the row-walking forward but rows under several bias
+    planes: the one-unit kernel runs; oracle parity of the whole call."""
+    w, x = make_inputs(128, 256, 4, 8, "bf16", rpb=64, seed=23)
+    print("\n[case] several planes at scale", flush=True)
+    got = gpu_run(x, "bf16", w.rows_per_bias)
+    ref = oracle_run(x, "bf16", w.rows_per_bias)
+    compare(got, ref, "bf16", label="several planes")
 
 
 @pytest.mark.parametrize("case", ROWS, ids=lambda c: "N%dL%dH%dd%d" % c[:4])

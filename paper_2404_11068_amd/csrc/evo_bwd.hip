@@ -922,14 +922,16 @@ BwdPlan plan_bwd(const Problem &p, bool has_bias, size_t cap) {
         const long v = env ? atol(env) : 0;
         return v > 0 ? (int64_t)v : (int64_t)4096;
     }();
-    // Row chunks of at least four rows: with fewer rows per workgroup the
-    // per-workgroup staging and the reduction of the partial planes cost more
-    // than the extra workgroups gain (16 rows over 8 heads: 4 chunks beat 8)
+    // With 8-wave or larger workgroups, row chunks of at least four rows:
+    // with fewer rows per workgroup the per-workgroup staging of a 256-key row
+    // and the reduction of the partial planes cost more than the extra
+    // workgroups gain (16 rows over 8 heads: 4 chunks beat 8; one-wave
+    // workgroups of 32-key rows gain from every extra chunk instead)
     int64_t chunks = 0;
     if (planes > 0 && rpb > 0 && nqt > 0) {
         const int64_t per_chunk = planes * p.H * nqt * waves * head_halves(p);  // waves per row chunk
         chunks = (target_waves + per_chunk - 1) / per_chunk;
-        if (chunks > rpb / 4) chunks = rpb / 4;
+        if (waves >= 8 && chunks > rpb / 4) chunks = rpb / 4;
         if (chunks < 1) chunks = 1;
         if (chunks > rpb) chunks = rpb;
     }

@@ -37,6 +37,10 @@
  *   call, since evo_attn_bwd_workspace_size and evo_attn_bwd must see the
  *   same value); and the fixed scratch of evo_attn_bwd_noalloc (below), with
  *   its per-device address, looked up on the first such call on a device.
+ *   One more environment variable is read on every evo_attn_fwd call and
+ *   kept nowhere: EVO_ATTN_FWD_ROWS=0 selects the one-(row, head)-per-
+ *   workgroup forward where the row-walking one (bias rows held in registers
+ *   across the rows of one head) would run; both give the same bits.
  * - Token tensors Q, K, V, G, O, dO, dQ, dK, dV, dG share one layout: element
  *   (r, t, h, c) lives at  base + r*stride_row + t*stride_tok + h*head_dim + c
  *   (strides in ELEMENTS; the [H, d] block of a token is contiguous).  The

@@ -696,8 +696,10 @@ hipError_t launch_q(const Problem &p, const FwdPtrs &x, hipStream_t s) {
 
 // Row-walking kernel: eligible when every row uses one bias plane, rows are
 // 16-byte aligned (bf16, L % 8 == 0), at most 256 keys, and there are at
-// least two units per resident workgroup (one 8-wave workgroup per CU at
-// the kernel's two waves per SIMD: 256 CUs x 8 waves).  EVO_ATTN_FWD_ROWS=0
+// least eight units per resident workgroup (one 8-wave workgroup per CU at
+// the kernel's two waves per SIMD: 256 CUs x 8 waves).  With fewer, the
+// bias held in registers is reused too few times to pay for the halved
+// occupancy: the one-unit kernel was as fast or faster at two to four.  EVO_ATTN_FWD_ROWS=0
 // in the environment at the time of the call selects the one-unit kernel
 // instead (same results; read on every call, no state kept).
 constexpr int64_t kRowsResidentWaves = 256 * 8;
@@ -731,7 +733,7 @@ hipError_t launch_t(const Problem &p, const FwdPtrs &x, hipStream_t s) {
         // and of the head count (every workgroup keeps one head)
         const int64_t g0 = kRowsResidentWaves / NKT;
         const int64_t g = g0 / 8 / p.H * 8 * p.H;
-        if (x.bias != nullptr && p.rpb >= p.N && g > 0 && units >= 2 * g0 && p.N < (int64_t(1) << 31) &&
+        if (x.bias != nullptr && p.rpb >= p.N && g > 0 && units >= 8 * g0 && p.N < (int64_t(1) << 31) &&
             fwd_rows_enabled())
             return launch_rows<D, NKT>(p, x, s, g);
     }

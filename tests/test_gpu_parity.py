@@ -85,27 +85,27 @@ def test_small_ragged_parity(case):
 
 
 # Shapes that select the row-walking forward (all rows under one bias plane,
-# bf16, L a multiple of 8, at most 256 keys, at least two (row, head) units
-# per resident workgroup): it must produce the bits of the one-unit kernel,
-# which the environment switch EVO_ATTN_FWD_ROWS=0 selects.  The full-size
-# workloads with a shared bias (MSA row, triangle, extra-MSA) run it against
-# the oracle in test_full_workload_parity.
+# bf16, L a multiple of 8, at most 256 keys, at least eight (row, head) units
+# per resident workgroup: 256 * 8 / (key tiles) workgroups): it must produce
+# the bits of the one-unit kernel, which the environment switch
+# EVO_ATTN_FWD_ROWS=0 selects.  The extra-MSA workload runs it against the
+# oracle in test_full_workload_parity.
 ROWS = [
     # N, L, H, d, kwargs
-    (128, 256, 4, 32, dict()),                      # 8 key tiles, 512 units
-    (64, 200, 8, 8, dict(p=0.2)),                   # ragged last key tile
-    (96, 248, 8, 16, dict(gate=False, mask="length")),
-    (256, 104, 4, 16, dict(mask="none")),           # 4 key tiles
-    (512, 40, 4, 8, dict(mask="tail_pad")),         # 2 key tiles
-    (1024, 24, 4, 32, dict()),                      # 1 key tile
-    (200, 256, 3, 16, dict(mask="length")),         # 3 heads: a grid of 240 workgroups
+    (512, 256, 4, 32, dict()),                      # 8 key tiles, 2048 units
+    (256, 200, 8, 8, dict(p=0.2)),                  # ragged last key tile
+    (256, 248, 8, 16, dict(gate=False, mask="length")),
+    (1024, 104, 4, 16, dict(mask="none")),          # 4 key tiles
+    (2048, 40, 4, 8, dict(mask="tail_pad")),        # 2 key tiles
+    (4096, 24, 4, 32, dict()),                      # 1 key tile
+    (700, 256, 3, 16, dict(mask="length")),         # 3 heads: a grid of 240 workgroups
 ]
 
 
 def test_forward_with_several_bias_planes_at_scale():
     """Enough units for the row-walking forward but rows under several bias
     planes: the one-unit kernel runs; oracle parity of the whole call."""
-    w, x = make_inputs(128, 256, 4, 8, "bf16", rpb=64, seed=23)
+    w, x = make_inputs(512, 256, 4, 8, "bf16", rpb=256, seed=23)
     print("\n[case] several planes at scale", flush=True)
     got = gpu_run(x, "bf16", w.rows_per_bias)
     ref = oracle_run(x, "bf16", w.rows_per_bias)

@@ -60,7 +60,7 @@ def forward_kernel(w, es: int) -> str:
     """The forward kernel the library runs for this workload: the row-walking
     kernel (bias rows held in registers across the rows of one head) for bf16
     at head_dim <= 32 and at most 256 keys in 16-byte rows, when all rows
-    share one bias plane and there are at least eight (row, head) units per
+    share one bias plane and there are at least two (row, head) units per
     resident workgroup; the one-unit kernel otherwise."""
     if es != 2 or w.head_dim > 32 or not w.bias or w.seq_len % 8 or w.seq_len > 256:
         return "fwd_kernel"
@@ -72,7 +72,7 @@ def forward_kernel(w, es: int) -> str:
     g0 = 256 * 8 // nkt
     g = g0 // 8 // w.n_heads * 8 * w.n_heads
     units = w.n_rows * w.n_heads
-    return "fwd_rows_kernel" if g > 0 and units >= 8 * g0 else "fwd_kernel"
+    return "fwd_rows_kernel" if g > 0 and units >= 2 * g0 else "fwd_kernel"
 
 
 def kernel_model(w, es: int, ws_bytes: int):

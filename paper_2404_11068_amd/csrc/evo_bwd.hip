@@ -495,15 +495,20 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(4
     const rsrc_t none = make_buf(nullptr, 0u);
     const float c2 = a.scale * kLog2e;
 
-    // bias tile of (this query tile, this key tile), constant over rows, in
-    // base-2 exponent units: reg i <-> key kt*32 + krow(i, h2)
-    float btl[16];
+    // bias tile of (this query tile, this key tile), constant over rows, as
+    // the starting value of the S^T tile: sqrt(d) * bias in fp32, so that
+    // c2 * S is the logit in base-2 units; reg i <-> key kt*32 + krow(i, h2)
+    f32x16 bacc;
     {
         const rsrc_t rb = a.bias ? make_buf((const E *)a.bias + (b * a.H + hh) * (int64_t)L * L, (uint32_t)(L * L * ES))
                                  : none;
+        float btl[16];
         load_bias16<T, BV>(rb, qvalid ? (uint32_t)(qi * L + kt * 32 + 8 * h2) : kOOB / ES, btl);
+        float sq_hi, sq_lo;
+        sqrt_split(D, sq_hi, sq_lo);
+        const float sqd = sq_hi + sq_lo;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) btl[i] *= kLog2e;
+        for (int i = 0; i < 16; ++i) bacc[i] = sqd * btl[i];
     }
     f32x16 acc = zero16();
 
@@ -601,8 +606,8 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(4
                 va.load(&v_lds[(kt * 32 + sig(n)) * KSTR], h2);
             }
             const float l2 = lse2_lds[n], ds = dsum_lds[n];
-            // S^T = K Q^T, dP^T = V dA^T: lane = query, reg i = key kt*32 + krow(i, h2)
-            f32x16 S = zero16(), dP = zero16();
+            // S^T = K Q^T + sqrt(d) bias^T, dP^T = V dA^T: lane = query, reg i = key kt*32 + krow(i, h2)
+            f32x16 S = bacc, dP = zero16();
             ChFrag<T, D>::mma(S, ka, qb);
             if constexpr (kTr) {
                 if (kbits != 0xffffffffu) {  // masked keys: -2^64 on their rows (row n is key sig(n))
@@ -615,7 +620,7 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(4
             f32x16 dS;
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
-                float p = __builtin_amdgcn_exp2f(__builtin_fmaf(S[i], c2, btl[i] - l2));
+                float p = __builtin_amdgcn_exp2f(__builtin_fmaf(S[i], c2, -l2));
                 if (!kTr && kbits != 0xffffffffu) p = __builtin_amdgcn_inverse_ballot_w64(
                                                   ((kbits >> krow(i, 0)) & 1u ? 0x00000000ffffffffull : 0ull) |
                                                   ((kbits >> krow(i, 1)) & 1u ? 0xffffffff00000000ull : 0ull))

@@ -88,6 +88,20 @@ __device__ __forceinline__ Tr<bf16_t>::K32 bias_k32(rsrc_t rb, int qi, int kt, i
     return f;
 }
 
+// A bias fragment as the starting value of a logit tile: register i holds
+// sqd * bias of key krow(i, h) -- the k32 slot order is the accumulator's
+// register order -- in fp32, one rounding of the product.  Passed as the C
+// operand of the tile's first QK^T product, it adds the scaled pair bias
+// without any bias product on the matrix unit.
+__device__ __forceinline__ f32x16 bias_acc(const Tr<bf16_t>::K32 &b, float sqd) {
+    f32x16 c;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int s = 0; s < 8; ++s) c[8 * t + s] = sqd * (float)b.v[t][s];
+    return c;
+}
+
 // 64-lane mask of the lanes whose logit register i belongs to a kept key:
 // register i of lane half h holds key krow(i, h) of the tile.
 __device__ __forceinline__ uint64_t key_lanes(uint32_t kb, int i) {
@@ -238,12 +252,6 @@ __global__ void __launch_bounds__(NKT / QG * 64) fwd_kernel(FwdArgs a) {
     const float c2 = a.scale * kLog2e;
     float sq_hi, sq_lo;
     sqrt_split(D, sq_hi, sq_lo);
-    const bool two_term = sq_lo != 0.0f;
-    K32 dhi{}, dlo{};
-    if constexpr (kBf) {
-        dhi = diag_k32(sq_hi, lane);
-        if (two_term) dlo = diag_k32(sq_lo, lane);
-    }
     const float sqd = sq_hi + sq_lo;
     __syncthreads();
 
@@ -284,13 +292,13 @@ __global__ void __launch_bounds__(NKT / QG * 64) fwd_kernel(FwdArgs a) {
             ChFrag<T, D> kf;
             kf.load(&k_lds[(kt * 32 + sig(n)) * KSTR], h2);
             s[kc] = zero16();
+            if constexpr (kBf) {
+                if constexpr (BV) bt = bcur[kc];
+                if (has_bias) s[kc] = bias_acc(bt, sqd);
+            }
             ChFrag<T, D>::mma(s[kc], kf, qf);
-            if (has_bias) {
-                if constexpr (kBf) {
-                    if constexpr (BV) bt = bcur[kc];
-                    Tr<bf16_t>::mma_k32(s[kc], dhi, bt);
-                    if (two_term) Tr<bf16_t>::mma_k32(s[kc], dlo, bt);
-                } else {
+            if constexpr (!kBf) {
+                if (has_bias) {
 #pragma unroll
                     for (int i = 0; i < 16; ++i) s[kc][i] = __builtin_fmaf(bf[i], sqd, s[kc][i]);
                 }
@@ -467,10 +475,7 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(2
     const float c2 = a.scale * kLog2e;
     float sq_hi, sq_lo;
     sqrt_split(D, sq_hi, sq_lo);
-    const bool two_term = sq_lo != 0.0f;
-    const K32 dhi = diag_k32(sq_hi, lane);
-    K32 dlo{};
-    if (two_term) dlo = diag_k32(sq_lo, lane);
+    const float sqd = sq_hi + sq_lo;
     // B operand of the masked-key term: 1 in k-slot 0 (lane half 0), zeros
     // elsewhere, so only the A operand's slot 0 (the key's mask word) counts
     const short4v mask_b = {h2 == 0 ? kBf16One : (short)0, 0, 0, 0};
@@ -497,13 +502,14 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(2
     };
 
     // ---- this wave's bias rows (query tile `wave`, every key tile), once;
-    // the host guarantees a single plane: plane 0 for every row
-    K32 breg[NKT];
+    // the host guarantees a single plane: plane 0 for every row.  They are
+    // kept as the fp32 starting values of the logit tiles (sqrt(d) * bias)
+    f32x16 bacc[NKT];
     {
         const rsrc_t rb = u < a.n_units ? make_buf((const E *)a.bias + (int64_t)uh * L * L, (uint32_t)(L * L * 2))
                                         : none;
 #pragma unroll
-        for (int kt = 0; kt < NKT; ++kt) breg[kt] = bias_k32<true>(rb, qi, kt, L, h2);
+        for (int kt = 0; kt < NKT; ++kt) bacc[kt] = bias_acc(bias_k32<true>(rb, qi, kt, L, h2), sqd);
     }
 
     // ---- the in-flight unit's K, V, key-mask byte and query tile
@@ -593,10 +599,8 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(2
             }
             const uint32_t kb = kbs[kt];
             if (kb != 0) {
-                f32x16 s = zero16();
+                f32x16 s = bacc[kt];
                 ChFrag<T, D>::mma(s, kf, qf);
-                Tr<bf16_t>::mma_k32(s, dhi, breg[kt]);
-                if (two_term) Tr<bf16_t>::mma_k32(s, dlo, breg[kt]);
                 if (kb != 0xffffffffu) {
                     // masked keys: -2^64 on their rows (row n of the tile is key sig(n))
                     const u32x2 mw = {mwv, 0u};
@@ -696,10 +700,9 @@ hipError_t launch_q(const Problem &p, const FwdPtrs &x, hipStream_t s) {
 
 // Row-walking kernel: eligible when every row uses one bias plane, rows are
 // 16-byte aligned (bf16, L % 8 == 0), at most 256 keys, and there are at
-// least eight units per resident workgroup (one 8-wave workgroup per CU at
-// the kernel's two waves per SIMD: 256 CUs x 8 waves).  With fewer, the
-// bias held in registers is reused too few times to pay for the halved
-// occupancy: the one-unit kernel was as fast or faster at two to four.  EVO_ATTN_FWD_ROWS=0
+// least two units per resident workgroup (one 8-wave workgroup per CU at
+// the kernel's two waves per SIMD: 256 CUs x 8 waves); with one, the bias
+// held in registers would not be reused at all.  EVO_ATTN_FWD_ROWS=0
 // in the environment at the time of the call selects the one-unit kernel
 // instead (same results; read on every call, no state kept).
 constexpr int64_t kRowsResidentWaves = 256 * 8;
@@ -733,7 +736,7 @@ hipError_t launch_t(const Problem &p, const FwdPtrs &x, hipStream_t s) {
         // and of the head count (every workgroup keeps one head)
         const int64_t g0 = kRowsResidentWaves / NKT;
         const int64_t g = g0 / 8 / p.H * 8 * p.H;
-        if (x.bias != nullptr && p.rpb >= p.N && g > 0 && units >= 8 * g0 && p.N < (int64_t(1) << 31) &&
+        if (x.bias != nullptr && p.rpb >= p.N && g > 0 && units >= 2 * g0 && p.N < (int64_t(1) << 31) &&
             fwd_rows_enabled())
             return launch_rows<D, NKT>(p, x, s, g);
     }

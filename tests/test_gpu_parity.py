@@ -85,14 +85,16 @@ def test_small_ragged_parity(case):
 
 
 # Shapes that select the row-walking forward (all rows under one bias plane,
-# bf16, L a multiple of 8, at most 256 keys, at least eight (row, head) units
+# bf16, L a multiple of 8, at most 256 keys, at least two (row, head) units
 # per resident workgroup: 256 * 8 / (key tiles) workgroups): it must produce
 # the bits of the one-unit kernel, which the environment switch
-# EVO_ATTN_FWD_ROWS=0 selects.  The extra-MSA workload runs it against the
-# oracle in test_full_workload_parity.
+# EVO_ATTN_FWD_ROWS=0 selects.  The full-size workloads with a shared bias
+# (MSA row, triangle, extra-MSA) run it against the oracle in
+# test_full_workload_parity.
 ROWS = [
     # N, L, H, d, kwargs
-    (512, 256, 4, 32, dict()),                      # 8 key tiles, 2048 units
+    (128, 256, 4, 32, dict()),                      # 8 key tiles, 512 units: the threshold
+    (512, 256, 4, 32, dict()),                      # 2048 units
     (256, 200, 8, 8, dict(p=0.2)),                  # ragged last key tile
     (256, 248, 8, 16, dict(gate=False, mask="length")),
     (1024, 104, 4, 16, dict(mask="none")),          # 4 key tiles

@@ -306,6 +306,11 @@ __global__ void __launch_bounds__(NKT / KG * 64) kv_kernel(KvArgs a) {
     }
     const bool kvalid = kin && (!has_mask || mbyte != 0);
     const bool kfull = __ballot(kvalid) == ~0ull;
+    // bf16: a masked key's logits get -2^64 from a rank-1 term on its lane's
+    // column, so its P is exactly 0 (one small MFMA per tile, issued in every
+    // tile: cheaper than a select per logit, and a branch around it costs
+    // registers)
+    const short mask_neg = kvalid ? (short)0 : kBf16MaskNeg;
     const float c2 = a.scale * kLog2e;
     const int arow = sig(n);  // permuted A-operand row of this lane
     uint16_t *const bt_tile = &bt_lds[kBD ? wave * 1024 : 0];  // (per wave of this workgroup)
@@ -323,13 +328,15 @@ __global__ void __launch_bounds__(NKT / KG * 64) kv_kernel(KvArgs a) {
             if constexpr (kBD) bias_block_load(rbt, L, qt + 1, kt, lane, braw);
             else load_bias16<T, BV>(rbt, bt_e0 + 32u * (qt + 1), bnext);
         }
-        // S = Q K^T and dP = dA V^T for 32 queries x this wave's 32 keys;
-        // lane = key, reg i = query qt*32 + krow(i, h2)
+        // S = Q K^T (plus the masked-key term) and dP = dA V^T for 32
+        // queries x this wave's 32 keys; lane = key, reg i = query
+        // qt*32 + krow(i, h2)
         ChFrag<T, D> qa, daa;
         qa.load(&q_lds[(qt * 32 + arow) * RSTR], h2);
         daa.load(&da_lds[(qt * 32 + arow) * RSTR], h2);
         f32x16 S = zero16(), dP = zero16();
         ChFrag<T, D>::mma(S, qa, kb);
+        if constexpr (kTr) mma_rank1(S, kBf16One, mask_neg, h2);
         ChFrag<T, D>::mma(dP, daa, vb);
         f32x16 P, dS;
 #pragma unroll
@@ -345,10 +352,12 @@ __global__ void __launch_bounds__(NKT / KG * 64) kv_kernel(KvArgs a) {
                 const int i = 8 * half + s8;
                 // log2 P = c2 * S + log2(e) * bias - lse * log2(e)
                 float p = __builtin_amdgcn_exp2f(__builtin_fmaf(S[i], c2, __builtin_fmaf(bcur[i], kLog2e, -l2[s8])));
-                // masked key: its lane's P is exactly 0.  A select, not a
-                // product: the lse leaves masked keys out, so exp2 of a masked
-                // logit far above it is +inf, and inf * 0 would be NaN
-                if (!kfull) p = kvalid ? p : 0.0f;
+                // fp32 masked key: its lane's P is exactly 0.  A select, not
+                // a product: the lse leaves masked keys out, so exp2 of a
+                // masked logit far above it is +inf, and inf * 0 would be NaN
+                if constexpr (!kTr) {
+                    if (!kfull) p = kvalid ? p : 0.0f;
+                }
                 P[i] = p;
                 dS[i] = p * (dP[i] - ds[s8]);
             }
@@ -612,7 +621,12 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(4
             if constexpr (kTr) {
                 if (kbits != 0xffffffffu) {  // masked keys: -2^64 on their rows (row n is key sig(n))
                     const short mv = ((kbits >> sig(n)) & 1u) ? (short)0 : kBf16MaskNeg;
-                    mma_rank1(S, mv, kBf16One, h2);
+                    // the lane half from an opaque copy, so that the term's
+                    // constant operand is formed here: hoisted out of the row
+                    // loop it is spilled at this kernel's register cap, and its
+                    // reload waits for every load and store in flight
+                    const int hq = (int)(opaque_u32((uint32_t)lane) >> 5);
+                    mma_rank1(S, mv, kBf16One, hq);
                 }
             }
             ChFrag<T, D>::mma(dP, va, dab);

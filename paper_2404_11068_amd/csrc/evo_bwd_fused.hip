@@ -168,10 +168,10 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
             return make_buf((const E *)X + r * a.srow + (int64_t)hh * D, row_bytes);
         };
         // per-row opaque copies of the lane's bias-row offset (query sig(n) of
-        // tile 0, this wave's keys) and thread index: each query tile's bias
+        // tile 0, this wave's keys) and lane index: each query tile's bias
         // and dQ addresses are formed from them inside the tile's step
         const uint32_t boff = opaque_u32((uint32_t)((sig(n) * L + kt * 32 + 8 * h2) * ES));
-        const int tid_r = (int)opaque_u32((uint32_t)tid);
+        const uint32_t lane_r = opaque_u32((uint32_t)lane);
         // ---- every load of the row goes out first, in the order of use
         ChFrag<bf16_t, D> kb, vb;
         kb.load(tok_buf(a.k), key_off, h2);
@@ -351,15 +351,22 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
                 }
             }
             __syncthreads();
-            // the sum of tile qt is taken by the threads from wave qt % NKT on
-            const int rot = (tid_r + NT - (qt % NKT) * 64) % NT;
+            // the sum of tile qt is taken by the waves from wave qt % NKT on,
+            // as many as its 8·D four-channel groups need: a wave-uniform
+            // test, so the other waves skip the index arithmetic and the
+            // reads.  Every wave still issues its store (off the end of the
+            // buffer where it has nothing to write), so that the count of
+            // loads and stores in flight is the same on both sides of the test
+            const uint32_t wr = (uint32_t)(wave + NKT - qt % NKT) % NKT;
 #pragma unroll
             for (int j = 0; j < NSUM; ++j) {  // four consecutive channels per thread and step
-                const int idx = rot + j * NT;
-                const int q = idx / (D / 4), cq = idx % (D / 4);
-                const bool ok = idx < 32 * (D / 4);
-                f32x4 sum = {0.0f, 0.0f, 0.0f, 0.0f};
-                if (ok) {
+                const uint32_t base = wr * 64u + (uint32_t)(j * NT);  // wave-uniform
+                u32x2 w2 = {0u, 0u};
+                uint32_t off = kOOB;
+                if (base < (uint32_t)(32 * (D / 4))) {
+                    const uint32_t idx = base + lane_r;
+                    const int q = (int)(idx / (D / 4)), cq = (int)(idx % (D / 4));
+                    f32x4 sum = {0.0f, 0.0f, 0.0f, 0.0f};
                     // partials read four at a time and added as fixed trees
                     constexpr int G = NKT < 4 ? NKT : 4;
 #pragma unroll
@@ -374,13 +381,10 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
                             for (int w = 0; w + st < G; w += 2 * st) x[w] += x[w + st];
                         sum += x[0];
                     }
+                    if (qt * 32 + q < L) off = (uint32_t)(qt * 32 + q) * stok_b + (uint32_t)(4 * cq * ES);
+                    w2.x = (uint32_t)f2bf(sum.x * a.scale) | ((uint32_t)f2bf(sum.y * a.scale) << 16);
+                    w2.y = (uint32_t)f2bf(sum.z * a.scale) | ((uint32_t)f2bf(sum.w * a.scale) << 16);
                 }
-                const uint32_t off = (ok && qt * 32 + q < L)
-                                         ? (uint32_t)(qt * 32 + q) * stok_b + (uint32_t)(4 * cq * ES)
-                                         : kOOB;
-                u32x2 w2;
-                w2.x = (uint32_t)f2bf(sum.x * a.scale) | ((uint32_t)f2bf(sum.y * a.scale) << 16);
-                w2.y = (uint32_t)f2bf(sum.z * a.scale) | ((uint32_t)f2bf(sum.w * a.scale) << 16);
                 __builtin_amdgcn_raw_buffer_store_b64(w2, rdq, off, 0, 0);
             }
         }

@@ -405,23 +405,6 @@ __device__ __forceinline__ uint32_t opaque_u32(uint32_t x) {
 }
 
 // ---------------------------------------------------------------------------
-// Constant A operand "c times a permuted identity" for the k32 contraction:
-// A[m][k] = c where k-slot k holds row sig(m) of the tile, else 0.  With a B
-// operand holding X[k][n] (k = key row of the tile, n = query), the product
-// adds c * X[sig(m)][n] to the D layout whose register i holds row krow(i, h)
-// -- i.e. it adds c times a [query][key] tile (read along keys) to logits
-// produced with sig-permuted key rows.  Used to fold the pair bias into the
-// MFMA accumulator.
-__device__ __forceinline__ Tr<bf16_t>::K32 diag_k32(float c, int lane) {
-    const int r = sig(lane & 31), h = lane >> 5;
-    Tr<bf16_t>::K32 f;
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int s = 0; s < 8; ++s) f.v[t][s] = (__bf16)((r == 16 * t + 8 * h + s) ? c : 0.0f);
-    return f;
-}
-
 // Constant B operand "c times the identity" for the k32 contraction:
 // B[k][n] = c where k == n.  With an A operand holding X[m][k] (k = key of
 // the tile, rows in any order), the product adds c * X[m][n] to the tile --

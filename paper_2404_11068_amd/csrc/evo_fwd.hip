@@ -64,8 +64,8 @@ struct FwdArgs {
     float scale;
 };
 
-// raw bf16 pair bias of key tile kt for query row qi, as the B operand of the
-// bias MFMA: k-slots {8h+s, 16+8h+s} = keys kt*32 + those slots.  Rows past L
+// raw bf16 pair bias of key tile kt for query row qi, in the k32 slot order:
+// slots {8h+s, 16+8h+s} = keys kt*32 + those slots.  Rows past L
 // read zeros; keys past L read the next row's values (those keys are masked,
 // so the values never matter).  BV: L % 8 == 0, rows are 16-byte aligned.
 template <bool BV>

@@ -140,8 +140,12 @@ def algorithmic_bytes(w, es: int):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    # the GPU's clock rises over the first ~30 ms of continuous work after an
+    # idle period (a step of the triangle workload: ~140 us in its first 50
+    # steps, ~116 us from about step 250 on), so the untimed warm-up runs 300
+    # steps by default and the timed steps see the clock a training loop runs at
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=300)
     ap.add_argument("--workload", default="tri_start_bf16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-baseline duration")

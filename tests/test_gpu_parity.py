@@ -131,6 +131,37 @@ def test_row_walking_forward_matches_one_unit_kernel(case, monkeypatch):
     assert torch.equal(lse0, lse1)
 
 
+# dBias sums dS over the R rows that share a plane.  Each row's term carries
+# the bf16 rounding of D (formed from the saved bf16 output) and of dA, and
+# where the softmax puts its mass on one key the exact term nearly cancels,
+# so those elements keep an absolute error that grows like sqrt(R) while
+# their reference stays near zero.  The normwise error does not grow
+# (measured 1.9e-3 from R = 64 to 2048); the element bound is met up to the
+# workloads' 256 rows per plane at head_dim 32 and 2048 at head_dim 8.
+_MANY_ROWS = [(1024, 32), (2048, 8)]
+
+
+@pytest.mark.parametrize("R,d", _MANY_ROWS, ids=lambda v: str(v))
+def test_dbias_over_many_rows_normwise(R, d):
+    w, x = make_inputs(R, 256, 4, d, "bf16", seed=77)
+    print("\n[case] dbias over rows", R, d, flush=True)
+    got = gpu_run(x, "bf16", w.rows_per_bias)
+    ref = oracle_run(x, "bf16", w.rows_per_bias)
+    compare(got, ref, "bf16", names=[n for n in ref if n != "dbias"], label="R%d d%d" % (R, d))
+    rel = np.linalg.norm(got["dbias"] - ref["dbias"]) / np.linalg.norm(ref["dbias"])
+    assert rel <= 1e-2, rel
+
+
+@pytest.mark.xfail(reason="bf16 dBias over 1024 rows at head_dim 32: near-cancelling elements keep a "
+                          "sqrt(R)-growing absolute error past the element bound (stated in evo_attn.h)",
+                   strict=False)
+def test_dbias_over_many_rows_elementwise():
+    w, x = make_inputs(1024, 256, 4, 32, "bf16", seed=77)
+    print("\n[case] dbias over rows, element bound", flush=True)
+    compare(gpu_run(x, "bf16", w.rows_per_bias), oracle_run(x, "bf16", w.rows_per_bias), "bf16",
+            names=["dbias"], label="R1024 d32")
+
+
 @pytest.mark.parametrize("d", [32, 64])
 def test_ending_node_transposed_view(d):
     """Triangle attention around the ending node: rows are the columns of the

@@ -235,29 +235,33 @@ def test_masked_keys_get_exact_zero_gradients():
     assert (got["dk"][masked] == 0).all() and (got["dv"][masked] == 0).all()
 
 
-@pytest.mark.parametrize("dtype,d", [("bf16", 8), ("bf16", 32), ("f32", 16)])
-def test_masked_keys_with_huge_logits(dtype, d):
+# 90 keys: the single-pass backward for bf16, the two-pass one for fp32; 256
+# keys at head_dim 16 and 32: the two-pass backward for bf16 (kv's masked-key
+# term on the matrix unit)
+@pytest.mark.parametrize("dtype,d,L", [("bf16", 8, 90), ("bf16", 32, 90), ("f32", 16, 90),
+                                       ("bf16", 32, 256), ("bf16", 16, 256)])
+def test_masked_keys_with_huge_logits(dtype, d, L):
     """Masked keys whose logits sit more than 100 above every kept key's are
     still excluded: exp of such a logit against the saved lse (which leaves
     masked keys out) overflows to +inf, so any multiply-by-zero masking would
     turn it into NaN.  One bias plane per row carries +120 at that row's
     masked keys; dK, dV and dBias must be exactly 0 there, and every output
     must match the oracle."""
-    N, L, H = 3, 90, 2
+    N, H = 3, 2
     w, x = make_inputs(N, L, H, d, dtype, seed=55 + d, rpb=1, p=0.3)
     masked = x["mask"] == 0
     assert masked.any()
     b = W.as_float64(x["bias"], dtype) + 120.0 * masked[:, None, None, :]
     x = dict(x)
     x["bias"] = W.f32_to_bf16_bits(b.astype(np.float32)) if dtype == "bf16" else b.astype(np.float32)
-    print("\n[case] masked keys, huge logits", dtype, d, flush=True)
+    print("\n[case] masked keys, huge logits", dtype, d, L, flush=True)
     got = gpu_run(x, dtype, w.rows_per_bias)
     for n in ("dk", "dv"):
         assert (got[n][masked] == 0).all(), n
     db = got["dbias"]  # [N, H, L, L]: plane r belongs to row r, its last axis is the key
     assert (db[np.broadcast_to(masked[:, None, None, :], db.shape)] == 0).all()
     ref = oracle_run(x, dtype, w.rows_per_bias)
-    compare(got, ref, dtype, label="huge masked logits %s d%d" % (dtype, d))
+    compare(got, ref, dtype, label="huge masked logits %s d%d L%d" % (dtype, d, L))
 
 
 def test_empty_problems_are_noops():

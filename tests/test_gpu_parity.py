@@ -60,6 +60,12 @@ SMALL = [
     # their reduction, one chunk per plane (dBias written directly), no bias
     (96, 256, 8, 8, "bf16", dict()),
     (128, 128, 8, 32, "bf16", dict(rpb=16, mask="length")),
+    # the dQ sum's wave split: one key tile at head_dim 32 (four summing steps
+    # per thread), two at head_dim 16 (both waves sum), four at head_dim 8
+    # (one of the four sums)
+    (4, 20, 2, 32, "bf16", dict()),
+    (4, 50, 2, 16, "bf16", dict(rpb=2)),
+    (4, 110, 2, 8, "bf16", dict(mask="tail_pad")),
     (64, 96, 2, 16, "bf16", dict(p=0.2)),
     (3, 200, 2, 8, "bf16", dict(rpb=1)),
     (5, 256, 3, 8, "bf16", dict(bias=False, gate=False)),

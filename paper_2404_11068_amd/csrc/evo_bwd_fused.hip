@@ -251,6 +251,14 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
         const uint64_t kbal = __ballot(kvalid);
         const bool kfull = kbal == ~0ull, kany = kbal != 0ull;
         const short mask_neg = kvalid ? (short)0 : kBf16MaskNeg;  // rank-1 term on this lane's key column
+        // the bias term of query tile 0 (sqrt(d) * bias through the matrix
+        // unit), formed while the staging barrier is waited for; each later
+        // tile's is formed before the previous tile's dQ barrier
+        f32x16 T = zero16();
+        if constexpr (HB) {
+            Tr<bf16_t>::mma_k32(T, bnext, eye_hi);
+            if (two_term) Tr<bf16_t>::mma_k32(T, bnext, eye_lo);
+        }
         __syncthreads();
 
         f32x16 dv_acc = zero16(), dk_acc = zero16();
@@ -260,9 +268,7 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
             if (qt >= nqt) break;
             float *const dq_part = dqp[qt & 1];
             // the next tile's bias rows go out first (loads complete in order)
-            K32 bcur;
             if constexpr (HB) {
-                bcur = bnext;
                 if (qt + 1 < NKT) {
                     if constexpr (BV) bnext = bias_rows_k32_at(rb, boff + (uint32_t)((qt + 1) * 32 * L * ES));
                     else bnext = bias_rows_k32<BV>(rb, L, qt + 1, kt, lane);
@@ -270,21 +276,17 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
             }
             f32x16 dq = zero16();
             if (kany) {
-                // raw logits S = Q K^T + sqrt(d) * bias (bias through the
-                // matrix unit, sqrt(d) as one or two bf16 terms; masked keys
-                // get -2^64 from a rank-1 term) and dP = dA V^T, for 32
-                // queries x this wave's 32 keys; lane = key, reg i = query
-                // qt*32 + krow(i, h2)
-                f32x16 S = zero16(), dP = zero16();
+                // raw logits S = sqrt(d) * bias + Q K^T (the bias term T was
+                // formed on the matrix unit before this tile, sqrt(d) as one
+                // or two bf16 terms; masked keys get -2^64 from a rank-1
+                // term) and dP = dA V^T, for 32 queries x this wave's 32
+                // keys; lane = key, reg i = query qt*32 + krow(i, h2)
+                f32x16 S = T, dP = zero16();
                 {
                     ChFrag<bf16_t, D> qa, daa;
                     qa.load(&q_lds[(qt * 32 + sig(n)) * RSTR], h2);
                     daa.load(&da_lds[(qt * 32 + sig(n)) * RSTR], h2);
                     ChFrag<bf16_t, D>::mma(S, qa, kb);
-                    if constexpr (HB) {
-                        Tr<bf16_t>::mma_k32(S, bcur, eye_hi);
-                        if (two_term) Tr<bf16_t>::mma_k32(S, bcur, eye_lo);
-                    }
                     if (!kfull) mma_rank1(S, kBf16One, mask_neg, h2);
                     ChFrag<bf16_t, D>::mma(dP, daa, vb);
                 }
@@ -348,6 +350,15 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
                     const f32x4 x1 = {dq[8 * half + 4], dq[8 * half + 5], dq[8 * half + 6], dq[8 * half + 7]};
                     *reinterpret_cast<f32x4 *>(&dq_part[dqs_index<D>(wave * 32 + n, n, c0 / 4)]) = x0;
                     *reinterpret_cast<f32x4 *>(&dq_part[dqs_index<D>(wave * 32 + n, n, c0 / 4 + 1)]) = x1;
+                }
+            }
+            // the next tile's bias term, on the matrix unit while this wave
+            // waits at the dQ barrier
+            if constexpr (HB) {
+                if (qt + 1 < NKT) {
+                    T = zero16();
+                    Tr<bf16_t>::mma_k32(T, bnext, eye_hi);
+                    if (two_term) Tr<bf16_t>::mma_k32(T, bnext, eye_lo);
                 }
             }
             __syncthreads();

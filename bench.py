@@ -1049,7 +1049,7 @@ def rate_calibration(torch, steps: int):
         out[name] = {"tera_lane_ops_per_s": round(blocks * 256 * 8 * iters / (ms * 1e-3) / 1e12, 2), "ms": round(ms, 4)}
     assert bool(torch.isfinite(sink).all())
     print(json.dumps({"rate_calibration": out, "lane_ops_per_launch": blocks * 256 * 8 * iters,
-                      "note": "8 independent chains per lane; median of %d launches" % steps}))
+                      "note": "8 independent chains per lane, one instruction per step; median of %d launches" % steps}))
 
 
 def copy_calibration(torch, mib: int, steps: int):

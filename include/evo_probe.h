@@ -24,7 +24,8 @@ enum evo_probe_op {
 /*
  * Enqueue one probe launch on `stream`: `n_blocks` workgroups of 256 threads,
  * each thread running 8 independent chains of `iters` operations of kind
- * `op` (so the launch retires n_blocks * 256 * 8 * iters lane operations).
+ * `op`, one instruction per chain step (so the launch retires
+ * n_blocks * 256 * 8 * iters lane operations of that instruction alone).
  * `sink` is caller-owned device memory of at least n_blocks * 256 floats; one
  * result per thread is written there so the work cannot be optimised away.
  * Returns 0, 1 (invalid argument: unknown op, n_blocks < 1, iters < 1, NULL

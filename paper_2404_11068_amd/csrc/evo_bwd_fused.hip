@@ -99,6 +99,14 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
     constexpr int RSTR = D + VEC;      // row stride of the Q, dA and K tiles in LDS (elements)
     constexpr int NST = (LP * CPT + NT - 1) / NT;           // staged 16-byte chunks per thread
     constexpr int NSUM = (32 * (D / 4) + NT - 1) / NT;      // 4-channel groups of dQ summed per thread
+    // head_dim 8: S and dP on the k=16 instruction, whose k-slots 8..15 carry
+    // the masked-key term (1 in each Q row's slot 8, the key's -2^64 or 0 in
+    // the K operand's) and -Dsum (each dA row's slots 8..10 hold -Dsum as
+    // three bf16 terms, the V operand's are 1): S comes with the mask and dP
+    // as dP - Dsum, so dS is one multiply per logit
+    constexpr bool kPad8 = D == 8;
+    using QKF = typename QKFragSel<bf16_t, D>::type;
+    static_assert(!kPad8 || CPT == 1, "one 16-byte chunk per token");
     __shared__ __attribute__((aligned(16))) E q_lds[LP * RSTR];
     __shared__ __attribute__((aligned(16))) E da_lds[LP * RSTR];
     __shared__ __attribute__((aligned(16))) E k_lds[LP * RSTR];
@@ -173,9 +181,14 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
         const uint32_t boff = opaque_u32((uint32_t)((sig(n) * L + kt * 32 + 8 * h2) * ES));
         const uint32_t lane_r = opaque_u32((uint32_t)lane);
         // ---- every load of the row goes out first, in the order of use
-        ChFrag<bf16_t, D> kb, vb;
-        kb.load(tok_buf(a.k), key_off, h2);
-        vb.load(tok_buf(a.v), key_off, h2);
+        QKF kb, vb;
+        if constexpr (kPad8) {
+            kb.load(tok_buf(a.k), key_off, h2, (short)0);  // slot 8: the mask word, set below
+            vb.load(tok_buf(a.v), key_off, h2, 0x3F803F80u, 0x00003F80u);  // slots 8..10: 1
+        } else {
+            kb.load(tok_buf(a.k), key_off, h2);
+            vb.load(tok_buf(a.v), key_off, h2);
+        }
         const uint32_t mbyte = bload1(has_mask ? make_buf(a.mask + r * a.L, (uint32_t)L) : none, (uint32_t)key);
         const float lraw = __builtin_bit_cast(
             float, bload4(make_buf(a.lse + (r * a.H + hh) * L, (uint32_t)L * 4u), tid < L ? (uint32_t)tid * 4u : kOOB));
@@ -233,24 +246,37 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
                     if (c == 0) dsum_lds[t] = valid ? part : 0.0f;
                     *reinterpret_cast<u32x4 *>(&q_lds[t * RSTR + c]) = qv[j];
                     *reinterpret_cast<u32x4 *>(&da_lds[t * RSTR + c]) = dav;
+                    if constexpr (kPad8) {
+                        // slots 8..15: Q (1, 0, ...), dA (-Dsum as hi + mid + lo, 0, ...)
+                        const float dsv = valid ? part : 0.0f;
+                        const uint16_t dh = f2bf(dsv);
+                        const float r1 = dsv - bf2f(dh);
+                        const uint16_t dm = f2bf(r1);
+                        const uint16_t dl = f2bf(r1 - bf2f(dm));
+                        const u32x4 qp = {(uint32_t)(uint16_t)kBf16One, 0u, 0u, 0u};
+                        const u32x4 dp = {((uint32_t)dh | ((uint32_t)dm << 16)) ^ 0x80008000u, (uint32_t)dl ^ 0x8000u, 0u, 0u};
+                        *reinterpret_cast<u32x4 *>(&q_lds[t * RSTR + 8]) = qp;
+                        *reinterpret_cast<u32x4 *>(&da_lds[t * RSTR + 8]) = dp;
+                    }
                 }
             }
             if (tid < LP)  // padded or fully masked queries: P = 0
                 lse2_lds[tid] = (tid < L && lraw != -INFINITY) ? lraw * kLog2e : INFINITY;
             // this wave's key rows of K, for the K^T operand of the dQ product
             E *krow_p = &k_lds[key * RSTR];
-            if constexpr (D >= 16) {
+            if constexpr (kPad8) {
+                *reinterpret_cast<bf16x8 *>(krow_p + 8 * h2) = kb.v;  // slots 8..15 are never read
+            } else {
 #pragma unroll
                 for (int kk = 0; kk < D / 16; ++kk)
                     *reinterpret_cast<bf16x8 *>(krow_p + 16 * kk + 8 * h2) = kb.v[kk];
-            } else {
-                *reinterpret_cast<short4v *>(krow_p + 4 * h2) = kb.v;
             }
         }
         const bool kvalid = kin && (!has_mask || mbyte != 0);
         const uint64_t kbal = __ballot(kvalid);
         const bool kfull = kbal == ~0ull, kany = kbal != 0ull;
         const short mask_neg = kvalid ? (short)0 : kBf16MaskNeg;  // rank-1 term on this lane's key column
+        if constexpr (kPad8) kb.set_slot8(h2, mask_neg);
         // the bias term of query tile 0 (sqrt(d) * bias through the matrix
         // unit), formed while the staging barrier is waited for; each later
         // tile's is formed before the previous tile's dQ barrier
@@ -283,22 +309,27 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
                 // keys; lane = key, reg i = query qt*32 + krow(i, h2)
                 f32x16 S = T, dP = zero16();
                 {
-                    ChFrag<bf16_t, D> qa, daa;
+                    QKF qa, daa;
                     qa.load(&q_lds[(qt * 32 + sig(n)) * RSTR], h2);
                     daa.load(&da_lds[(qt * 32 + sig(n)) * RSTR], h2);
-                    ChFrag<bf16_t, D>::mma(S, qa, kb);
-                    if (!kfull) mma_rank1(S, kBf16One, mask_neg, h2);
-                    ChFrag<bf16_t, D>::mma(dP, daa, vb);
+                    QKF::mma(S, qa, kb);
+                    if (!kPad8 && !kfull) mma_rank1(S, kBf16One, mask_neg, h2);
+                    QKF::mma(dP, daa, vb);
                 }
                 f32x16 P, dS;
 #pragma unroll
                 for (int half = 0; half < 2; ++half) {
                     const int q0 = qt * 32 + 16 * half + 8 * h2;
                     const f32x4 *lp = reinterpret_cast<const f32x4 *>(&lse2_lds[q0]);
-                    const f32x4 *dp = reinterpret_cast<const f32x4 *>(&dsum_lds[q0]);
-                    const f32x4 l0 = lp[0], l1 = lp[1], d0 = dp[0], d1 = dp[1];
+                    const f32x4 l0 = lp[0], l1 = lp[1];
                     const float l2[8] = {l0.x, l0.y, l0.z, l0.w, l1.x, l1.y, l1.z, l1.w};
-                    const float ds[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+                    float ds[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};  // in dP already at head_dim 8
+                    if constexpr (!kPad8) {
+                        const f32x4 *dp = reinterpret_cast<const f32x4 *>(&dsum_lds[q0]);
+                        const f32x4 d0 = dp[0], d1 = dp[1];
+                        ds[0] = d0.x; ds[1] = d0.y; ds[2] = d0.z; ds[3] = d0.w;
+                        ds[4] = d1.x; ds[5] = d1.y; ds[6] = d1.z; ds[7] = d1.w;
+                    }
 #pragma unroll
                     for (int s8 = 0; s8 < 8; ++s8) {
                         const int i = 8 * half + s8;
@@ -306,7 +337,7 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
                         // S_raw is below -2^63, so its P is exactly 0
                         const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(S[i], c2, -l2[s8]));
                         P[i] = p;
-                        dS[i] = p * (dP[i] - ds[s8]);
+                        dS[i] = kPad8 ? p * dP[i] : p * (dP[i] - ds[s8]);
                     }
                 }
                 if constexpr (HB) {

@@ -228,6 +228,44 @@ template <> struct ChFrag<bf16_t, 8> {
     }
 };
 
+// bf16, D = 8 on the k=16 instruction, which on gfx950 issues in about 80% of
+// the time of the k=8 one: lane half 0 holds the 8 channels, lane half 1
+// k-slots 8..15, which carry one extra rank-1 term of the product.  An LDS row
+// of 16 elements holds the 8 channels and then the row's slots 8..15; a token
+// loaded from memory gets `slot8` in slot 8 and zeros after it.
+struct Frag8K16 {
+    bf16x8 v;
+    __device__ __forceinline__ void load(rsrc_t r, uint32_t tok, int h, short slot8) {
+        u32x4 x = bload16(r, h == 0 ? tok : kOOB);
+        x.x = h == 0 ? x.x : (uint32_t)(uint16_t)slot8;
+        v = __builtin_bit_cast(bf16x8, x);
+    }
+    // as above with slots 8..11 of lane half 1 given as two words (low half first)
+    __device__ __forceinline__ void load(rsrc_t r, uint32_t tok, int h, uint32_t w0, uint32_t w1) {
+        u32x4 x = bload16(r, h == 0 ? tok : kOOB);
+        x.x = h == 0 ? x.x : w0;
+        x.y = h == 0 ? x.y : w1;
+        v = __builtin_bit_cast(bf16x8, x);
+    }
+    // slot 8 (lane half 1) set after the load
+    __device__ __forceinline__ void set_slot8(int h, short s8) {
+        u32x4 x = __builtin_bit_cast(u32x4, v);
+        x.x = h == 0 ? x.x : (uint32_t)(uint16_t)s8;
+        v = __builtin_bit_cast(bf16x8, x);
+    }
+    __device__ __forceinline__ void load(const uint16_t *row, int h) {
+        v = *reinterpret_cast<const bf16x8 *>(row + 8 * h);
+    }
+    __device__ __forceinline__ static void mma(f32x16 &acc, const Frag8K16 &a, const Frag8K16 &b) {
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.v, b.v, acc, 0, 0, 0);
+    }
+};
+
+// operand fragment of a product over the head channels: bf16 at D = 8 takes
+// the k=16 form above
+template <typename T, int D> struct QKFragSel { using type = ChFrag<T, D>; };
+template <> struct QKFragSel<bf16_t, 8> { using type = Frag8K16; };
+
 // ---------------------------------------------------------------------------
 // k32 A operand of a contraction over 32 rows of a row-major bf16 LDS tile X
 // (X[row][col], `stride` elements per row), where the operand's row m is

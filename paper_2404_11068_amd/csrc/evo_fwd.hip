@@ -142,6 +142,13 @@ __global__ void __launch_bounds__(NKT / QG * 64) fwd_kernel(FwdArgs a) {
     constexpr int NPF = (LP * CPT + NT - 1) / NT;  // 16-byte chunks of K (and of V) per thread
     constexpr int NBB = kBf && BV ? KC : 1;    // bias fragments per chunk held in registers
     constexpr int NG = ES == 2 ? 1 : 2;        // 16-byte gate loads per 8 channels
+    // bf16 at head_dim 8: the logit product runs on the k=16 instruction; each
+    // K row in LDS is followed by its k-slots 8..15 (the key's masked-key word,
+    // then zeros) and each query has a 1 in slot 8, so the product also adds
+    // -2^64 on masked keys and no separate masked-key term is needed
+    constexpr bool kPad8 = kBf && D == 8;
+    using QKF = typename QKFragSel<T, D>::type;
+    static_assert(!kPad8 || (CPT == 1 && NPF == NKB), "one K chunk and one mask byte per key and thread step");
     __shared__ __attribute__((aligned(16))) E k_lds[LP * KSTR];
     __shared__ __attribute__((aligned(16))) E v_lds[kBf ? LP * VSTRB : DO * VSTR];
     __shared__ uint32_t kbits[NKT];
@@ -196,6 +203,11 @@ __global__ void __launch_bounds__(NKT / QG * 64) fwd_kernel(FwdArgs a) {
             if (idx < LP * CPT) {
                 const int t = idx / CPT, c = (idx % CPT) * VEC;
                 *reinterpret_cast<u32x4 *>(&k_lds[t * KSTR + c]) = kr[j];
+                if constexpr (kPad8) {
+                    const bool keep = (!has_mask || mb[j] != 0) && t < L;
+                    const u32x4 w = {keep ? 0u : (uint32_t)(uint16_t)kBf16MaskNeg, 0u, 0u, 0u};
+                    *reinterpret_cast<u32x4 *>(&k_lds[t * KSTR + 8]) = w;
+                }
                 const int cv = c - c_off;  // V: only the unit's output channels
                 if (NHALF == 1 || (cv >= 0 && cv < DO)) {
                     if constexpr (kBf) {
@@ -228,8 +240,9 @@ __global__ void __launch_bounds__(NKT / QG * 64) fwd_kernel(FwdArgs a) {
             }
         }
     }
-    ChFrag<T, D> qf;
-    qf.load(tok_buf(a.q), q_off, h2);
+    QKF qf;
+    if constexpr (kPad8) qf.load(tok_buf(a.q), q_off, h2, kBf16One);
+    else qf.load(tok_buf(a.q), q_off, h2);
     // bias of the first chunk, then the gate (needed last)
     K32 bcur[NBB];
     if constexpr (kBf && BV) {
@@ -289,14 +302,14 @@ __global__ void __launch_bounds__(NKT / QG * 64) fwd_kernel(FwdArgs a) {
             const uint32_t kb = __builtin_amdgcn_readfirstlane(kbits[kt]);
             kbs[kc] = kb;
             if (kb == 0) continue;
-            ChFrag<T, D> kf;
+            QKF kf;
             kf.load(&k_lds[(kt * 32 + sig(n)) * KSTR], h2);
             s[kc] = zero16();
             if constexpr (kBf) {
                 if constexpr (BV) bt = bcur[kc];
                 if (has_bias) s[kc] = bias_acc(bt, sqd);
             }
-            ChFrag<T, D>::mma(s[kc], kf, qf);
+            QKF::mma(s[kc], kf, qf);
             if constexpr (!kBf) {
                 if (has_bias) {
 #pragma unroll
@@ -304,7 +317,9 @@ __global__ void __launch_bounds__(NKT / QG * 64) fwd_kernel(FwdArgs a) {
                 }
             }
             if (kb != 0xffffffffu) {
-                if constexpr (kBf) {
+                if constexpr (kPad8) {
+                    // the masked-key term came with the product
+                } else if constexpr (kBf) {
                     // masked keys: -2^64 on their rows (row n of the tile is key sig(n))
                     const short mv = ((kb >> sig(n)) & 1u) ? (short)0 : kBf16MaskNeg;
                     mma_rank1(s[kc], mv, kBf16One, h2);
@@ -455,6 +470,11 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(2
     constexpr int PCH = (32 - D) / 8;          // constant 16-byte chunks per V row
     constexpr bool kOnesRow = D < 32;          // row sums come out of the PV product
     constexpr int NPF = (LP * CPT + NT - 1) / NT;
+    // head_dim 8: the logit product on the k=16 instruction, the masked-key
+    // word in each K row's slot 8 (as in the one-unit kernel)
+    constexpr bool kPad8 = D == 8;
+    using QKF = typename QKFragSel<T, D>::type;
+    static_assert(!kPad8 || NPF == 1, "one K chunk per key, staged by the thread of that key");
     __shared__ __attribute__((aligned(16))) E k_lds[LP * KSTR];
     __shared__ __attribute__((aligned(16))) E v_lds[LP * VSTRB];
     __shared__ uint32_t mneg_lds[LP];          // masked-key operand per key: -2^64 (bf16, low half) or 0
@@ -515,7 +535,7 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(2
     // ---- the in-flight unit's K, V, key-mask byte and query tile
     u32x4 kr[NPF], vr[NPF];
     uint32_t mr;
-    ChFrag<T, D> qn;
+    QKF qn;
     auto issue_unit = [&](int64_t rr, int h, bool ok) {
         const int64_t tb = rr * a.srow + (int64_t)h * D;
         const rsrc_t rk = tok_buf(a.k, tb, ok), rv = tok_buf(a.v, tb, ok);
@@ -529,7 +549,8 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(2
         }
         const rsrc_t rm = (has_mask && ok) ? make_buf(a.mask + rr * a.L, (uint32_t)L) : none;
         mr = bload1(rm, (uint32_t)tid);
-        qn.load(tok_buf(a.q, tb, ok), q_off, h2);
+        if constexpr (kPad8) qn.load(tok_buf(a.q, tb, ok), q_off, h2, kBf16One);
+        else qn.load(tok_buf(a.q, tb, ok), q_off, h2);
     };
 
     // every load is issued whether or not a mask or gate exists (an empty
@@ -545,6 +566,7 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(2
         const bool okn = u + G < a.n_units;
         __syncthreads();  // the previous unit's reads of the LDS tiles are done
         // ---- stage the unit: registers -> LDS, key-mask words and bits
+        const bool keep = (!has_mask || mr != 0) && tid < L;  // key tid
 #pragma unroll
         for (int j = 0; j < NPF; ++j) {
             const int idx = tid + j * NT;
@@ -552,18 +574,23 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(2
                 const int t = idx / CPT, c = (idx % CPT) * VEC;
                 *reinterpret_cast<u32x4 *>(&k_lds[t * KSTR + c]) = kr[j];
                 *reinterpret_cast<u32x4 *>(&v_lds[t * VSTRB + c]) = vr[j];
+                if constexpr (kPad8) {  // t == tid
+                    const u32x4 w = {keep ? 0u : (uint32_t)(uint16_t)kBf16MaskNeg, 0u, 0u, 0u};
+                    *reinterpret_cast<u32x4 *>(&k_lds[t * KSTR + 8]) = w;
+                }
             }
         }
         {
-            const bool keep = (!has_mask || mr != 0) && tid < L;
-            if (tid < LP) mneg_lds[tid] = keep ? 0u : (uint32_t)(uint16_t)kBf16MaskNeg;
+            if constexpr (!kPad8) {
+                if (tid < LP) mneg_lds[tid] = keep ? 0u : (uint32_t)(uint16_t)kBf16MaskNeg;
+            }
             const unsigned long long bal = __ballot(keep);
             if (lane == 0) {
                 if (2 * wave < NKT) kbits[2 * wave] = (uint32_t)bal;
                 if (2 * wave + 1 < NKT) kbits[2 * wave + 1] = (uint32_t)(bal >> 32);
             }
         }
-        const ChFrag<T, D> qf = qn;
+        const QKF qf = qn;
         __syncthreads();
 
         u32x4 graw = {0u, 0u, 0u, 0u}, graw2 = {0u, 0u, 0u, 0u};
@@ -576,18 +603,18 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(2
         uint32_t kbs[NKT];
 #pragma unroll
         for (int kt = 0; kt < NKT; ++kt) kbs[kt] = __builtin_amdgcn_readfirstlane(kbits[kt]);
-        ChFrag<T, D> kf_n;
+        QKF kf_n;
         kf_n.load(&k_lds[sig(n) * KSTR], h2);
-        uint32_t mw_n = mneg_lds[sig(n)];
+        uint32_t mw_n = kPad8 ? 0u : mneg_lds[sig(n)];
         K32 va_n = load_k32_tr(v_lds, VSTRB, 0, 32, lane);
 #pragma unroll
         for (int kt = 0; kt < NKT; ++kt) {
-            const ChFrag<T, D> kf = kf_n;
+            const QKF kf = kf_n;
             const uint32_t mwv = mw_n;
             const K32 va = va_n;
             if (kt + 1 < NKT) {
                 kf_n.load(&k_lds[((kt + 1) * 32 + sig(n)) * KSTR], h2);
-                mw_n = mneg_lds[(kt + 1) * 32 + sig(n)];
+                if constexpr (!kPad8) mw_n = mneg_lds[(kt + 1) * 32 + sig(n)];
                 va_n = load_k32_tr(v_lds, VSTRB, (kt + 1) * 32, 32, lane);
             }
             // ---- global loads, in the order they are waited for
@@ -600,8 +627,8 @@ __global__ void __launch_bounds__(NKT * 64) __attribute__((amdgpu_waves_per_eu(2
             const uint32_t kb = kbs[kt];
             if (kb != 0) {
                 f32x16 s = bacc[kt];
-                ChFrag<T, D>::mma(s, kf, qf);
-                if (kb != 0xffffffffu) {
+                QKF::mma(s, kf, qf);
+                if (!kPad8 && kb != 0xffffffffu) {
                     // masked keys: -2^64 on their rows (row n of the tile is key sig(n))
                     const u32x2 mw = {mwv, 0u};
                     s = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(__builtin_bit_cast(short4v, mw), mask_b, s, 0, 0, 0);

@@ -8,6 +8,10 @@ nothing from the product.
 The arithmetic lives in ``evo_attn_oracle.c`` (plain loops, fp64, OpenMP over
 (row, head) pairs); this file only builds and calls it through ctypes.
 Every function cites what it computes in the C source header.
+
+``EVO_ORACLE_LIB``, when set, names an already compiled oracle library to load
+instead of the one built here (the mutation test points it at copies of the C
+source with planted mistakes, to show that the pins catch them).
 """
 from __future__ import annotations
 
@@ -46,9 +50,12 @@ def build(force: bool = True) -> str:
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < max(map(os.path.getmtime, _SRCS)):
-            build(force=True)
-        lib = ctypes.CDLL(_LIB)
+        path = os.environ.get("EVO_ORACLE_LIB")
+        if not path:
+            path = _LIB
+            if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < max(map(os.path.getmtime, _SRCS)):
+                build(force=True)
+        lib = ctypes.CDLL(path)
         P = ctypes.c_void_p
         lib.evo_oracle_fwd.argtypes = [ctypes.POINTER(_Dims), P, P, P, P, P, P, P, P]
         lib.evo_oracle_bwd.argtypes = [ctypes.POINTER(_Dims)] + [P] * 12

@@ -305,8 +305,10 @@ __global__ void __launch_bounds__(NKT * 64) bwd_fused_kernel(FusedArgs a) {
                 // raw logits S = sqrt(d) * bias + Q K^T (the bias term T was
                 // formed on the matrix unit before this tile, sqrt(d) as one
                 // or two bf16 terms; masked keys get -2^64 from a rank-1
-                // term) and dP = dA V^T, for 32 queries x this wave's 32
-                // keys; lane = key, reg i = query qt*32 + krow(i, h2)
+                // term, at head_dim 8 from the product's k-slot 8) and
+                // dP = dA V^T (at head_dim 8 already less Dsum), for 32
+                // queries x this wave's 32 keys; lane = key, reg i = query
+                // qt*32 + krow(i, h2)
                 f32x16 S = T, dP = zero16();
                 {
                     QKF qa, daa;

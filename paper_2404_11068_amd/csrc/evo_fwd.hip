@@ -438,17 +438,18 @@ __global__ void __launch_bounds__(NKT / QG * 64) fwd_kernel(FwdArgs a) {
 // 32, at most 256 keys).  A fixed grid of workgroups, its size a multiple of
 // the head count, walks the units u, u + G, u + 2G, ... (G = grid size): all
 // units of a workgroup are rows of one head under the one bias plane.  Each
-// wave loads its query tile's bias rows once, into registers (the K32
-// operands of every key tile, about 64 registers at 256 keys), and reuses
-// them for every row it visits, so the pair bias leaves L2 once per
-// workgroup instead of once per (row, head).  The next unit's K, V, key mask
-// and query tile are requested during the current unit's first key tile and
-// held in registers until that unit is staged; the gate during the last key
-// tile; each key tile reads the next tile's K and V^T operands and mask word
-// from LDS before its own math.  Per-workgroup constants (the bias diagonal
-// operands, the constant columns of the V tile) are set up once.  Per key
-// tile, against the one-unit kernel above: the masked-key operand is one LDS
-// word (written at staging), the tile max is a chain of three-input maxima,
+// wave loads its query tile's bias rows once and keeps them in registers as
+// the fp32 starting values of its logit tiles (sqrt(d) * bias, 128 registers
+// at 256 keys), reused for every row it visits, so the pair bias leaves L2
+// once per workgroup instead of once per (row, head).  The next unit's K, V,
+// key mask and query tile are requested during the current unit's first key
+// tile and held in registers until that unit is staged; the gate during the
+// last key tile; each key tile reads the next tile's K and V^T operands and
+// mask word from LDS before its own math.  The constant columns of the V tile
+// are set up once per workgroup.  Per key tile, against the one-unit kernel
+// above: the masked-key operand is one LDS word (written at staging; at
+// head_dim 8 it rides in the logit product's spare k-slots, as in the one-unit
+// kernel), the tile max is a chain of three-input maxima,
 // the two lane halves exchange their maxima only when some lane's own
 // maximum calls for a raise of the reference max (no lane's own maximum
 // above the threshold means no combined one is), and the exponent offset

@@ -243,9 +243,10 @@ def test_masked_keys_get_exact_zero_gradients():
 
 # 90 keys: the single-pass backward for bf16, the two-pass one for fp32; 256
 # keys at head_dim 16 and 32: the two-pass backward for bf16 (kv's masked-key
-# term on the matrix unit)
+# term on the matrix unit); 256 keys at head_dim 8: the single pass with the
+# masked-key term and -Dsum in the logit and dP products' spare k-slots
 @pytest.mark.parametrize("dtype,d,L", [("bf16", 8, 90), ("bf16", 32, 90), ("f32", 16, 90),
-                                       ("bf16", 32, 256), ("bf16", 16, 256)])
+                                       ("bf16", 32, 256), ("bf16", 16, 256), ("bf16", 8, 256)])
 def test_masked_keys_with_huge_logits(dtype, d, L):
     """Masked keys whose logits sit more than 100 above every kept key's are
     still excluded: exp of such a logit against the saved lse (which leaves

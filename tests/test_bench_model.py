@@ -21,10 +21,12 @@ sys.path.insert(0, ROOT)
 import bench  # noqa: E402
 from paper_2404_11068_amd import workloads as W  # noqa: E402
 
+
 def _tensors(N, L, H, d, es, bias_planes, gate=True, mask=True):
     tok = N * L * H * d * es
     return dict(tok=tok, lse=N * H * L * 4, bias=bias_planes * H * L * L * es, dbias=bias_planes * H * L * L * 4,
                 mask=N * L if mask else 0, gates=1 if gate else 0)
+
 
 # name: (N, L, H, d, bytes per element, bias planes)
 SCOPE = {
@@ -34,6 +36,7 @@ SCOPE = {
     "tri_start_bf16": (256, 256, 4, 32, 2, 1),
     "extra_msa_bf16": (1024, 256, 8, 8, 2, 1),
 }
+
 
 @pytest.mark.parametrize("name", sorted(SCOPE))
 def test_algorithmic_bytes_are_the_tensors_of_the_method(name):
@@ -47,10 +50,12 @@ def test_algorithmic_bytes_are_the_tensors_of_the_method(name):
     bwd = (5 + t["gates"]) * t["tok"] + t["lse"] + t["bias"] + t["mask"] + (3 + t["gates"]) * t["tok"] + t["dbias"]
     assert bench.algorithmic_bytes(w, es) == (fwd, bwd)
 
+
 def test_headline_byte_counts():
     """The triangle workload: 85.52 MB forward and 170.46 MB backward."""
     fwd, bwd = bench.algorithmic_bytes(W.by_name("tri_start_bf16"), 2)
     assert (fwd, bwd) == (85_524_480, 170_459_136)
+
 
 # the kernels each workload runs, as the kernel traces in profiles/ show them
 TRACED = {
@@ -63,6 +68,7 @@ TRACED = {
     "extra_msa_bf16_share8": ("fwd_rows_kernel", True),
 }
 
+
 @pytest.mark.parametrize("name", sorted(TRACED))
 def test_launch_rules_match_the_traces(name):
     w = W.by_name(name)
@@ -74,6 +80,7 @@ def test_launch_rules_match_the_traces(name):
     assert fwd_name + "<" in prof
     assert ("bwd_fused_kernel<" in prof) == fused
     assert ("qbias_kernel<" in prof) == (not fused)
+
 
 @pytest.mark.parametrize("name", sorted(TRACED))
 def test_kernel_model_adds_up(name):
